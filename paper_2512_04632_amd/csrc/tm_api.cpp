@@ -1,0 +1,422 @@
+// C ABI of the Turbo-Muon orthogonalizer: argument validation, per-stream
+// workspace cache and the launch plan of Algorithms 1 and 2 (one launch per
+// phase over the tiles of every matrix of the call).
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <array>
+#include <cstdio>
+#include <cstdlib>
+#include <cstring>
+#include <map>
+#include <mutex>
+#include <string>
+#include <utility>
+#include <vector>
+
+#include "tm_internal.h"
+#include "turbomuon.h"
+
+namespace tmk {
+hipError_t launch_phase_bf16(int kind, int cfg, const Phase& P, hipStream_t st);
+hipError_t launch_phase_f32(int kind, int cfg, const Phase& P, hipStream_t st);
+}  // namespace tmk
+
+namespace {
+
+using tmk::Entry;
+using tmk::Phase;
+
+thread_local std::string g_last_error;
+
+tm_status fail(tm_status s, const std::string& msg) {
+  g_last_error = msg;
+  return s;
+}
+
+// Default coefficients: the constant quintic triple, used for every iteration.
+constexpr float kA = 3.4445f, kB = -4.7750f, kC = 2.0315f;
+
+struct Workspace {
+  void* ptr = nullptr;
+  size_t bytes = 0;
+};
+
+std::mutex g_mu;
+std::map<std::pair<int, hipStream_t>, Workspace> g_ws;
+std::map<int, bool> g_dev_ok;
+
+// Timing hooks: event pairs bracketing each launch while enabled.
+struct TimedLaunch {
+  int kind;
+  hipEvent_t start, stop;
+};
+bool g_timing = false;
+std::vector<TimedLaunch> g_timed;
+double g_time_ms[TM_NUM_PHASES];
+int64_t g_time_n[TM_NUM_PHASES];
+
+void collect_timing() {
+  for (TimedLaunch& t : g_timed) {
+    float ms = 0.f;
+    if (hipEventSynchronize(t.stop) == hipSuccess &&
+        hipEventElapsedTime(&ms, t.start, t.stop) == hipSuccess) {
+      g_time_ms[t.kind] += double(ms);
+      g_time_n[t.kind] += 1;
+    }
+    (void)hipEventDestroy(t.start);
+    (void)hipEventDestroy(t.stop);
+  }
+  g_timed.clear();
+}
+
+// One matrix (or a batch of equal matrices stored back to back).
+struct Item {
+  char* x;
+  uint32_t k, N;
+  uint32_t count;
+  bool tall;
+};
+
+tm_status check_device(int* dev) {
+  hipError_t e = hipGetDevice(dev);
+  if (e != hipSuccess) return fail(TM_ERR_HIP, std::string("hipGetDevice: ") + hipGetErrorString(e));
+  auto it = g_dev_ok.find(*dev);
+  if (it == g_dev_ok.end()) {
+    hipDeviceProp_t prop;
+    e = hipGetDeviceProperties(&prop, *dev);
+    if (e != hipSuccess)
+      return fail(TM_ERR_HIP, std::string("hipGetDeviceProperties: ") + hipGetErrorString(e));
+    const bool ok = std::strncmp(prop.gcnArchName, "gfx950", 6) == 0;
+    it = g_dev_ok.emplace(*dev, ok).first;
+  }
+  if (!it->second) return fail(TM_ERR_UNSUPPORTED, "device is not gfx950 (MI355X)");
+  return TM_OK;
+}
+
+// Grow the (device, stream) workspace to at least `bytes`.
+tm_status get_workspace(int dev, hipStream_t st, size_t bytes, char** out) {
+  Workspace& w = g_ws[{dev, st}];
+  if (w.bytes < bytes) {
+    if (w.ptr) {
+      hipError_t e = hipStreamSynchronize(st);
+      if (e != hipSuccess)
+        return fail(TM_ERR_HIP, std::string("hipStreamSynchronize: ") + hipGetErrorString(e));
+      (void)hipFree(w.ptr);
+      w.ptr = nullptr;
+      w.bytes = 0;
+    }
+    void* p = nullptr;
+    if (std::getenv("TM_TEST_FAIL_ALLOC") != nullptr ||
+        hipMalloc(&p, bytes) != hipSuccess || p == nullptr) {
+      (void)hipGetLastError();
+      return fail(TM_ERR_NO_MEMORY, "workspace allocation of " + std::to_string(bytes) +
+                                        " bytes failed");
+    }
+    w.ptr = p;
+    w.bytes = bytes;
+  }
+  *out = static_cast<char*>(w.ptr);
+  return TM_OK;
+}
+
+uint64_t item_ws(const Item& it, int esz) {
+  return tmk::ws_layout(it.k, it.N, uint32_t(esz)).total * it.count;
+}
+
+// Pick the largest tile whose launch still spans at least one wave of the
+// chip's 256 compute units; otherwise the smallest tile.
+int choose_cfg(int kind, const std::vector<Item>& items) {
+  for (int cfg = 0; cfg < tmk::kNumCfg - 1; ++cfg) {
+    uint64_t tiles = 0;
+    for (const Item& it : items) tiles += uint64_t(it.count) * tmk::blocks_per_matrix(kind, cfg, it.k, it.N);
+    if (tiles >= 256) return cfg;
+  }
+  return tmk::kNumCfg - 1;
+}
+
+struct Plan {
+  const std::vector<Item>* items;
+  std::vector<uint64_t> ws_off;   // byte offset of each item's workspace region
+  char* ws;
+  int esz;
+  hipStream_t st;
+};
+
+// One launch of `kind` per chunk of at most kMaxEntries items.
+tm_status launch(const Plan& pl, int kind, int cfg, int src, int dst, float a, float b, float c,
+                 uint32_t flags, int aux, bool tall_only) {
+  const std::vector<Item>& items = *pl.items;
+  for (size_t base = 0; base < items.size(); base += tmk::kMaxEntries) {
+    Phase P;
+    std::memset(&P, 0, sizeof(P));
+    const size_t n = std::min(items.size() - base, size_t(tmk::kMaxEntries));
+    uint64_t start = 0;
+    for (size_t i = 0; i < n; ++i) {
+      const Item& it = items[base + i];
+      Entry& E = P.e[i];
+      E.x = it.x;
+      E.ws = pl.ws_off[base + i];
+      E.k = it.k;
+      E.N = it.N;
+      E.count = it.count;
+      E.flags = it.tall ? tmk::kTall : 0u;
+      E.tile_start = uint32_t(start);
+      E.tiles_per = (tall_only && !it.tall) ? 0u : tmk::blocks_per_matrix(kind, cfg, it.k, it.N);
+      start += uint64_t(E.tiles_per) * it.count;
+    }
+    if (start >= (uint64_t(1) << 31))
+      return fail(TM_ERR_UNSUPPORTED, "too many tiles in one launch");
+    P.nent = int32_t(n);
+    P.total = int32_t(start);
+    P.ws = pl.ws;
+    P.src = src;
+    P.dst = dst;
+    P.a = a;
+    P.b = b;
+    P.c = c;
+    P.flags = flags;
+    P.aux = aux;
+    TimedLaunch tl{kind, nullptr, nullptr};
+    if (g_timing && P.total > 0) {
+      if (hipEventCreate(&tl.start) != hipSuccess || hipEventCreate(&tl.stop) != hipSuccess)
+        return fail(TM_ERR_HIP, "hipEventCreate failed");
+      (void)hipEventRecord(tl.start, pl.st);
+    }
+    const hipError_t e = pl.esz == 2 ? tmk::launch_phase_bf16(kind, cfg, P, pl.st)
+                                     : tmk::launch_phase_f32(kind, cfg, P, pl.st);
+    if (tl.start) {
+      (void)hipEventRecord(tl.stop, pl.st);
+      g_timed.push_back(tl);
+    }
+    if (e != hipSuccess)
+      return fail(TM_ERR_HIP, std::string("kernel launch: ") + hipGetErrorString(e));
+  }
+  return TM_OK;
+}
+
+tm_status run(std::vector<Item>& items, int esz, int iters, const float* coeffs, int precond,
+              hipStream_t st) {
+  if (items.empty()) return TM_OK;
+  std::lock_guard<std::mutex> lock(g_mu);
+  int dev = 0;
+  tm_status s = check_device(&dev);
+  if (s != TM_OK) return s;
+  Plan pl;
+  pl.items = &items;
+  pl.esz = esz;
+  pl.st = st;
+  uint64_t total = 0;
+  for (const Item& it : items) {
+    pl.ws_off.push_back(total);
+    total += item_ws(it, esz);
+  }
+  s = get_workspace(dev, st, size_t(total), &pl.ws);
+  if (s != TM_OK) return s;
+
+  bool any_tall = false;
+  for (const Item& it : items) any_tall = any_tall || it.tall;
+  if (any_tall && (iters > 0 || precond == TM_PRECOND_AOL)) {
+    s = launch(pl, tmk::kKindTransposeIn, 0, 0, 0, 0.f, 0.f, 0.f, 0u, 0, true);
+    if (s != TM_OK) return s;
+  }
+  const int gcfg = choose_cfg(tmk::kKindGram, items);
+  const int pcfg = choose_cfg(tmk::kKindPoly, items);
+  const int ucfg = choose_cfg(tmk::kKindUpdate, items);
+  const bool aol = precond == TM_PRECOND_AOL, frob = precond == TM_PRECOND_FROBENIUS;
+
+  if (frob) {  // Algorithm 1, first line: s = 1 / ||X0||_F
+    s = launch(pl, tmk::kKindFrob, 0, 0, 0, 0.f, 0.f, 0.f, 0u, 0, false);
+    if (s == TM_OK) s = launch(pl, tmk::kKindAolVector, 0, 0, 0, 0.f, 0.f, 0.f, tmk::kFrob, 0, false);
+    if (s != TM_OK) return s;
+  }
+  if (iters == 0) {
+    if (aol) {
+      s = launch(pl, tmk::kKindGram, gcfg, tmk::kSlotFirst, 0, 0.f, 0.f, 0.f,
+                 tmk::kRowSum | tmk::kA32, 0, false);
+      if (s == TM_OK)
+        s = launch(pl, tmk::kKindAolVector, 0, 0, 0, 0.f, 0.f, 0.f, 0u, tmk::cfg_tile(gcfg), false);
+      if (s != TM_OK) return s;
+    }
+    if (aol || frob) s = launch(pl, tmk::kKindApplyScale, 0, 0, 0, 0.f, 0.f, 0.f, 0u, 0, false);
+    return s;
+  }
+
+  int src = tmk::kSlotFirst;
+  for (int it = 1; it <= iters; ++it) {
+    const float a = coeffs ? coeffs[3 * (it - 1)] : kA;
+    const float b = coeffs ? coeffs[3 * (it - 1) + 1] : kB;
+    const float c = coeffs ? coeffs[3 * (it - 1) + 2] : kC;
+    // A single iteration would read and write the caller's buffer: it goes
+    // through W1 and a final copy instead.
+    const int dst = (it == iters && iters > 1) ? tmk::kSlotFinal
+                                               : (it % 2 == 1 ? tmk::kSlotAlt1 : tmk::kSlotAlt2);
+    const bool first = it == 1;
+    const uint32_t scale = (first && (aol || frob)) ? tmk::kScale : 0u;
+    const uint32_t gflags = ((first && aol) ? tmk::kRowSum : 0u) | (scale ? tmk::kA32 : 0u);
+    s = launch(pl, tmk::kKindGram, gcfg, src, 0, 0.f, 0.f, 0.f, gflags, 0, false);
+    if (s == TM_OK && first && aol)  // Algorithm 2, second line: the AOL vector
+      s = launch(pl, tmk::kKindAolVector, 0, 0, 0, 0.f, 0.f, 0.f, 0u, tmk::cfg_tile(gcfg), false);
+    if (s == TM_OK) s = launch(pl, tmk::kKindPoly, pcfg, 0, 0, a, b, c, scale, 0, false);
+    if (s == TM_OK) s = launch(pl, tmk::kKindUpdate, ucfg, src, dst, a, b, c, scale, 0, false);
+    if (s != TM_OK) return s;
+    src = dst;
+  }
+  if (iters == 1) s = launch(pl, tmk::kKindCopyOut, 0, src, 0, 0.f, 0.f, 0.f, 0u, 0, false);
+  return s;
+}
+
+tm_status check_common(int iters, const float* coeffs, int precond) {
+  if (iters < 0 || iters > TM_MAX_ITERS)
+    return fail(TM_ERR_INVALID_ARG, "iters out of range [0, " + std::to_string(TM_MAX_ITERS) + "]");
+  if (precond != TM_PRECOND_NONE && precond != TM_PRECOND_FROBENIUS && precond != TM_PRECOND_AOL)
+    return fail(TM_ERR_INVALID_ARG, "unknown precond " + std::to_string(precond));
+  (void)coeffs;
+  return TM_OK;
+}
+
+tm_status check_shape(int64_t m, int64_t n) {
+  if (m < 1 || n < 1 || m > TM_MAX_DIM || n > TM_MAX_DIM)
+    return fail(TM_ERR_INVALID_ARG, "matrix size " + std::to_string(m) + "x" + std::to_string(n) +
+                                        " out of range [1, " + std::to_string(TM_MAX_DIM) + "]");
+  return TM_OK;
+}
+
+Item make_item(void* X, int64_t m, int64_t n, int64_t count) {
+  Item it;
+  it.x = static_cast<char*>(X);
+  it.tall = m > n;
+  it.k = uint32_t(std::min(m, n));
+  it.N = uint32_t(std::max(m, n));
+  it.count = uint32_t(count);
+  return it;
+}
+
+tm_status batched(void* X, int64_t m, int64_t n, int64_t batch, int iters, const float* coeffs,
+                  int precond, void* stream, int esz) {
+  g_last_error.clear();
+  tm_status s = check_common(iters, coeffs, precond);
+  if (s != TM_OK) return s;
+  if (batch < 0) return fail(TM_ERR_INVALID_ARG, "batch < 0");
+  s = check_shape(m, n);
+  if (s != TM_OK) return s;
+  if (batch == 0) return TM_OK;
+  if (X == nullptr) return fail(TM_ERR_INVALID_ARG, "X is NULL");
+  if (reinterpret_cast<uintptr_t>(X) % uintptr_t(esz) != 0)
+    return fail(TM_ERR_UNSUPPORTED, "X is not aligned to its element size");
+  if (batch > INT32_MAX) return fail(TM_ERR_INVALID_ARG, "batch too large");
+  std::vector<Item> items{make_item(X, m, n, batch)};
+  return run(items, esz, iters, coeffs, precond, static_cast<hipStream_t>(stream));
+}
+
+tm_status grouped(void* const* X, const int64_t* m, const int64_t* n, int64_t count, int iters,
+                  const float* coeffs, int precond, void* stream, int esz) {
+  g_last_error.clear();
+  tm_status s = check_common(iters, coeffs, precond);
+  if (s != TM_OK) return s;
+  if (count < 0) return fail(TM_ERR_INVALID_ARG, "count < 0");
+  if (count == 0) return TM_OK;
+  if (X == nullptr || m == nullptr || n == nullptr)
+    return fail(TM_ERR_INVALID_ARG, "X, m or n is NULL");
+  std::vector<Item> items;
+  items.reserve(size_t(count));
+  for (int64_t g = 0; g < count; ++g) {
+    s = check_shape(m[g], n[g]);
+    if (s != TM_OK) return fail(s, "matrix " + std::to_string(g) + ": " + g_last_error);
+    if (X[g] == nullptr) return fail(TM_ERR_INVALID_ARG, "X[" + std::to_string(g) + "] is NULL");
+    if (reinterpret_cast<uintptr_t>(X[g]) % uintptr_t(esz) != 0)
+      return fail(TM_ERR_UNSUPPORTED, "X[" + std::to_string(g) + "] is not element aligned");
+    items.push_back(make_item(X[g], m[g], n[g], 1));
+  }
+  return run(items, esz, iters, coeffs, precond, static_cast<hipStream_t>(stream));
+}
+
+}  // namespace
+
+extern "C" {
+
+tm_status tm_orthogonalize(void* X, int64_t m, int64_t n, int64_t batch, int iters,
+                           const float* coeffs, int precond, void* stream) {
+  return batched(X, m, n, batch, iters, coeffs, precond, stream, 2);
+}
+
+tm_status tm_orthogonalize_f32(float* X, int64_t m, int64_t n, int64_t batch, int iters,
+                               const float* coeffs, int precond, void* stream) {
+  return batched(X, m, n, batch, iters, coeffs, precond, stream, 4);
+}
+
+tm_status tm_orthogonalize_grouped(void* const* X, const int64_t* m, const int64_t* n,
+                                   int64_t count, int iters, const float* coeffs, int precond,
+                                   void* stream) {
+  return grouped(X, m, n, count, iters, coeffs, precond, stream, 2);
+}
+
+tm_status tm_orthogonalize_grouped_f32(float* const* X, const int64_t* m, const int64_t* n,
+                                       int64_t count, int iters, const float* coeffs,
+                                       int precond, void* stream) {
+  return grouped(reinterpret_cast<void* const*>(X), m, n, count, iters, coeffs, precond, stream, 4);
+}
+
+uint64_t tm_workspace_bytes(const int64_t* m, const int64_t* n, int64_t count, int dtype_bytes) {
+  if (m == nullptr || n == nullptr || count < 0 || (dtype_bytes != 2 && dtype_bytes != 4)) return 0;
+  uint64_t total = 0;
+  for (int64_t g = 0; g < count; ++g) {
+    if (m[g] < 1 || n[g] < 1 || m[g] > TM_MAX_DIM || n[g] > TM_MAX_DIM) return 0;
+    total += item_ws(make_item(nullptr, m[g], n[g], 1), dtype_bytes);
+  }
+  return total;
+}
+
+tm_status tm_release_workspaces(void) {
+  std::lock_guard<std::mutex> lock(g_mu);
+  if (g_ws.empty()) return TM_OK;
+  hipError_t e = hipDeviceSynchronize();
+  for (auto& kv : g_ws)
+    if (kv.second.ptr) (void)hipFree(kv.second.ptr);
+  g_ws.clear();
+  if (e != hipSuccess) return fail(TM_ERR_HIP, std::string("hipDeviceSynchronize: ") + hipGetErrorString(e));
+  return TM_OK;
+}
+
+tm_status tm_timing_enable(int enable) {
+  std::lock_guard<std::mutex> lock(g_mu);
+  g_timing = enable != 0;
+  return TM_OK;
+}
+
+tm_status tm_timing_read(int phase, double* total_ms, int64_t* launches) {
+  if (phase < 0 || phase >= TM_NUM_PHASES || total_ms == nullptr || launches == nullptr)
+    return fail(TM_ERR_INVALID_ARG, "bad phase or null output");
+  std::lock_guard<std::mutex> lock(g_mu);
+  collect_timing();
+  *total_ms = g_time_ms[phase];
+  *launches = g_time_n[phase];
+  return TM_OK;
+}
+
+tm_status tm_timing_reset(void) {
+  std::lock_guard<std::mutex> lock(g_mu);
+  collect_timing();
+  for (int i = 0; i < TM_NUM_PHASES; ++i) {
+    g_time_ms[i] = 0.0;
+    g_time_n[i] = 0;
+  }
+  return TM_OK;
+}
+
+const char* tm_status_string(tm_status s) {
+  switch (s) {
+    case TM_OK: return "TM_OK";
+    case TM_ERR_INVALID_ARG: return "TM_ERR_INVALID_ARG";
+    case TM_ERR_UNSUPPORTED: return "TM_ERR_UNSUPPORTED";
+    case TM_ERR_NO_MEMORY: return "TM_ERR_NO_MEMORY";
+    case TM_ERR_HIP: return "TM_ERR_HIP";
+  }
+  return "TM_ERR_UNKNOWN";
+}
+
+const char* tm_last_error(void) { return g_last_error.c_str(); }
+
+const char* tm_version(void) { return "0.1.0"; }
+
+}  // extern "C"

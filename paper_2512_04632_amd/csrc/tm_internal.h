@@ -1,0 +1,119 @@
+// Shared between the host planner (tm_api.cpp) and the gfx950 kernels
+// (tm_kernels.hip): launch descriptors and the per-matrix workspace layout.
+#pragma once
+
+#include <stdint.h>
+
+#ifndef __HIPCC__
+#define TM_HD inline
+#else
+#define TM_HD __host__ __device__ inline
+#endif
+
+namespace tmk {
+
+TM_HD uint64_t align256(uint64_t v) { return (v + 255u) & ~uint64_t(255u); }
+TM_HD uint32_t cdiv(uint32_t a, uint32_t b) { return (a + b - 1u) / b; }
+TM_HD uint32_t kpad(uint32_t k) { return (k + 7u) & ~7u; }   // ld of A and B
+
+// Matrices of one launch are described by up to kMaxEntries entries; an entry
+// covers `count` matrices of one shape stored back to back (a batched call is
+// one entry, a grouped call one entry per matrix).  Bigger groups are split
+// into several launches per phase.
+constexpr int kMaxEntries = 64;
+
+// Y slots named by the phase descriptors.  A slot resolves per matrix:
+//   slot   wide (m <= n)          tall (m > n)
+//   0      user matrix (X1)       W1 (X^T copied in)
+//   1      W1                     W2
+//   2      W2                     W1
+//   3      user matrix            user matrix, stored transposed (N x k, ld = k)
+// Iteration 1 reads slot 0, iterations write 1, 2, 1, 2, ... and the last
+// one writes slot 3, so no update ever reads the buffer it writes.
+constexpr int kSlotFirst = 0;
+constexpr int kSlotAlt1 = 1;
+constexpr int kSlotAlt2 = 2;
+constexpr int kSlotFinal = 3;
+
+// Phase flags.
+constexpr uint32_t kScale = 1u;   // first iteration after AOL / Frobenius: apply s
+constexpr uint32_t kRowSum = 2u;  // Gram epilogue emits AOL row-sum partials
+constexpr uint32_t kFrob = 4u;    // AOL-vector kernel: uniform s from the Frobenius partials
+constexpr uint32_t kA32 = 8u;     // Gram stores A0 in fp32 (first iteration, before scaling)
+
+// Entry flags.
+constexpr uint32_t kTall = 1u;    // the user matrix is N x k (m > n); work on its transpose
+
+constexpr int kFrobBlocks = 32;   // partial sums of squares per matrix
+constexpr int kMinTile = 64;      // smallest Gram tile: bounds the row-sum partial count
+
+struct Entry {
+  char* x;             // user matrix of element 0
+  uint64_t ws;         // byte offset of element 0's workspace region
+  uint32_t k, N;       // wide view: k = min(m, n) rows, N = max(m, n) columns
+  uint32_t count;      // matrices in this entry
+  uint32_t flags;      // kTall
+  uint32_t tile_start; // first logical block of this entry in the launch
+  uint32_t tiles_per;  // blocks per matrix in the launch
+};
+
+struct Phase {
+  Entry e[kMaxEntries];
+  char* ws;            // workspace base
+  int32_t nent;
+  int32_t total;       // logical blocks in the launch
+  int32_t src, dst;    // Y slots
+  float a, b, c;       // coefficients of this iteration
+  uint32_t flags;
+  int32_t aux;         // AOL-vector kernel: tile size of the Gram that wrote the partials
+};
+
+// Tile configurations of the matrix-core kernels (square tiles, 256 threads).
+constexpr int kNumCfg = 3;
+TM_HD int cfg_tile(int cfg) { return cfg == 0 ? 256 : (cfg == 1 ? 128 : 64); }
+
+// Logical blocks per matrix of each kernel.
+enum Kind { kKindTransposeIn, kKindFrob, kKindGram, kKindAolVector, kKindPoly,
+            kKindUpdate, kKindApplyScale, kKindCopyOut };
+constexpr int kTransposeTile = 64;
+constexpr int kElemBlock = 2048;     // elements per block of the elementwise kernels
+
+TM_HD uint32_t tri(uint32_t nb) { return nb * (nb + 1u) / 2u; }
+
+TM_HD uint32_t blocks_per_matrix(int kind, int cfg, uint32_t k, uint32_t N) {
+  const uint32_t T = uint32_t(cfg_tile(cfg));
+  switch (kind) {
+    case kKindTransposeIn: return cdiv(k, kTransposeTile) * cdiv(N, kTransposeTile);
+    case kKindFrob: return uint32_t(kFrobBlocks);
+    case kKindGram:
+    case kKindPoly: return tri(cdiv(k, T));
+    case kKindAolVector: return cdiv(k, 256u);
+    case kKindUpdate: return cdiv(k, T) * cdiv(N, T);
+    case kKindApplyScale:
+    case kKindCopyOut: return uint32_t((uint64_t(k) * N + kElemBlock - 1) / kElemBlock);
+  }
+  return 0;
+}
+
+struct WsLayout {
+  uint64_t w1, w2, a, b, a32, s, part, fpart, total;
+};
+
+// Byte offsets of the sub-buffers of one matrix's workspace region.
+TM_HD WsLayout ws_layout(uint32_t k, uint32_t N, uint32_t esz) {
+  WsLayout L;
+  const uint64_t y = align256(uint64_t(k) * N * esz);
+  const uint64_t g = align256(uint64_t(k) * kpad(k) * esz);
+  L.w1 = 0;
+  L.w2 = L.w1 + y;
+  L.a = L.w2 + y;
+  L.b = L.a + g;
+  L.a32 = L.b + g;
+  L.s = L.a32 + align256(uint64_t(k) * kpad(k) * 4u);
+  L.part = L.s + align256(uint64_t(k) * 4u);
+  L.fpart = L.part + align256(uint64_t(cdiv(k, kMinTile)) * k * 4u);
+  L.total = L.fpart + align256(uint64_t(kFrobBlocks) * 4u);
+  return L;
+}
+
+}  // namespace tmk

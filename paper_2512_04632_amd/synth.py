@@ -118,3 +118,33 @@ def workload_shapes(name: str):
             out.append((m, n, alpha, i))
             i += 1
     return out
+
+
+def power_law_batch_device(count: int, m: int, n: int, alpha: float, seed: int,
+                           device="cuda", dtype=None, noise: float = 0.01):
+    """The same recipe drawn on the GPU with torch in float32 (benchmark inputs).
+
+    Used where the float64 host draw of large matrices would dominate the run
+    time (QR of 14336 x 4096 Gaussians); values differ from
+    ``power_law_matrix`` but follow the same distribution.  Returns a
+    (count, m, n) tensor cast once to ``dtype`` (default bfloat16).
+    """
+    import torch
+    dtype = torch.bfloat16 if dtype is None else dtype
+    g = torch.Generator(device=device)
+    g.manual_seed(int(seed))
+    k = min(m, n)
+    out = torch.empty((count, m, n), dtype=dtype, device=device)
+    sigma = torch.arange(1, k + 1, dtype=torch.float32, device=device) ** (-float(alpha))
+    for i in range(count):
+        gu = torch.randn((m, k), generator=g, device=device, dtype=torch.float32)
+        gv = torch.randn((n, k), generator=g, device=device, dtype=torch.float32)
+        qu, ru = torch.linalg.qr(gu)
+        qv, rv = torch.linalg.qr(gv)
+        qu = qu * torch.sign(torch.diagonal(ru)).clamp(min=0).mul(2).sub(1)[None, :]
+        qv = qv * torch.sign(torch.diagonal(rv)).clamp(min=0).mul(2).sub(1)[None, :]
+        e = torch.randn((m, n), generator=g, device=device, dtype=torch.float32)
+        x = (qu * sigma[None, :]) @ qv.T.contiguous() + noise * e
+        out[i].copy_(x.to(dtype))
+        del gu, gv, qu, qv, ru, rv, e, x
+    return out

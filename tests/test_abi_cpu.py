@@ -1,0 +1,117 @@
+"""The C ABI without a GPU: the library loads, exports every declared symbol
+and rejects invalid arguments before touching the HIP runtime."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2512_04632_amd import _lib as tm
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "turbomuon.h")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    return sorted(set(re.findall(r"^[A-Za-z_][\w ]*\*?\s*(tm_\w+)\s*\(", text, re.M)))
+
+
+def header_defines():
+    text = open(HEADER).read()
+    return {k: int(v) for k, v in re.findall(r"#define\s+(TM_\w+)\s+\(?(-?\d+)\)?", text)}
+
+
+def test_library_exports_every_declared_symbol():
+    names = declared_functions()
+    assert len(names) >= 9
+    L = tm.lib()
+    for name in names:
+        assert hasattr(L, name), name
+    assert set(names) == set(tm._SIGNATURES)
+
+
+def test_constants_match_header():
+    d = header_defines()
+    assert d["TM_OK"] == tm.TM_OK and d["TM_ERR_INVALID_ARG"] == tm.TM_ERR_INVALID_ARG
+    assert d["TM_ERR_UNSUPPORTED"] == tm.TM_ERR_UNSUPPORTED
+    assert d["TM_ERR_NO_MEMORY"] == tm.TM_ERR_NO_MEMORY and d["TM_ERR_HIP"] == tm.TM_ERR_HIP
+    assert d["TM_PRECOND_NONE"] == tm.PRECOND["none"]
+    assert d["TM_PRECOND_FROBENIUS"] == tm.PRECOND["frobenius"]
+    assert d["TM_PRECOND_AOL"] == tm.PRECOND["aol"]
+    assert d["TM_MAX_DIM"] == tm.TM_MAX_DIM and d["TM_MAX_ITERS"] == tm.TM_MAX_ITERS
+
+
+def test_status_strings_and_version():
+    for code, name in [(0, "TM_OK"), (-1, "TM_ERR_INVALID_ARG"), (-2, "TM_ERR_UNSUPPORTED"),
+                       (-3, "TM_ERR_NO_MEMORY"), (-4, "TM_ERR_HIP")]:
+        assert tm.status_string(code) == name
+    assert tm.status_string(7) == "TM_ERR_UNKNOWN"
+    assert re.fullmatch(r"\d+\.\d+\.\d+", tm.version())
+
+
+FAKE = ctypes.c_void_p(0x1000)   # never dereferenced: validation fails or batch = 0
+
+
+@pytest.mark.parametrize("fn", ["tm_orthogonalize", "tm_orthogonalize_f32"])
+@pytest.mark.parametrize("m,n,batch,iters,precond,code", [
+    (0, 4, 1, 4, 2, tm.TM_ERR_INVALID_ARG),
+    (4, 0, 1, 4, 2, tm.TM_ERR_INVALID_ARG),
+    (-3, 4, 1, 4, 2, tm.TM_ERR_INVALID_ARG),
+    (65537, 4, 1, 4, 2, tm.TM_ERR_INVALID_ARG),
+    (4, 4, -1, 4, 2, tm.TM_ERR_INVALID_ARG),
+    (4, 4, 1, -1, 2, tm.TM_ERR_INVALID_ARG),
+    (4, 4, 1, 65, 2, tm.TM_ERR_INVALID_ARG),
+    (4, 4, 1, 4, 3, tm.TM_ERR_INVALID_ARG),
+    (4, 4, 1, 4, -1, tm.TM_ERR_INVALID_ARG),
+    (4, 4, 0, 4, 2, tm.TM_OK),                 # empty batch: no-op
+])
+def test_batched_validation(fn, m, n, batch, iters, precond, code):
+    f = getattr(tm.lib(), fn)
+    assert f(FAKE, m, n, batch, iters, None, precond, None) == code
+    if code != tm.TM_OK:
+        assert tm.last_error() != ""
+
+
+def test_null_and_misaligned_pointers():
+    L = tm.lib()
+    assert L.tm_orthogonalize(None, 4, 4, 1, 4, None, 2, None) == tm.TM_ERR_INVALID_ARG
+    assert L.tm_orthogonalize(ctypes.c_void_p(0x1001), 4, 4, 1, 4, None, 2, None) == tm.TM_ERR_UNSUPPORTED
+    assert L.tm_orthogonalize_f32(ctypes.c_void_p(0x1002), 4, 4, 1, 4, None, 2, None) == tm.TM_ERR_UNSUPPORTED
+    # a null pointer with an empty batch is still a no-op
+    assert L.tm_orthogonalize(None, 4, 4, 0, 4, None, 2, None) == tm.TM_OK
+
+
+@pytest.mark.parametrize("fn", ["tm_orthogonalize_grouped", "tm_orthogonalize_grouped_f32"])
+def test_grouped_validation(fn):
+    f = getattr(tm.lib(), fn)
+    ptrs = (ctypes.c_void_p * 2)(0x1000, 0x2000)
+    ms = (ctypes.c_int64 * 2)(8, 16)
+    ns = (ctypes.c_int64 * 2)(8, 0)
+    assert f(ptrs, ms, ns, 2, 4, None, 2, None) == tm.TM_ERR_INVALID_ARG
+    assert "matrix 1" in tm.last_error()
+    ns[1] = 4
+    assert f(ptrs, ms, ns, 2, 4, None, 9, None) == tm.TM_ERR_INVALID_ARG
+    assert f(ptrs, ms, ns, -1, 4, None, 2, None) == tm.TM_ERR_INVALID_ARG
+    assert f(None, ms, ns, 2, 4, None, 2, None) == tm.TM_ERR_INVALID_ARG
+    nulls = (ctypes.c_void_p * 2)(0x1000, None)
+    assert f(nulls, ms, ns, 2, 4, None, 2, None) == tm.TM_ERR_INVALID_ARG
+    assert f(ptrs, ms, ns, 0, 4, None, 2, None) == tm.TM_OK
+
+
+def test_workspace_bytes():
+    # ping-pong Y twice, A and B (k x roundup8(k)), s, row-sum partials, Frobenius partials
+    def a256(v):
+        return (v + 255) // 256 * 256
+
+    def expect(m, n, e):
+        k, N = min(m, n), max(m, n)
+        kp = (k + 7) // 8 * 8
+        return (2 * a256(k * N * e) + 2 * a256(k * kp * e) + a256(4 * k * kp) + a256(4 * k)
+                + a256(4 * k * ((k + 63) // 64)) + a256(4 * 32))
+
+    shapes = [(768, 3072), (3072, 768), (17, 33), (1, 1)]
+    for e in (2, 4):
+        assert tm.workspace_bytes(shapes, e) == sum(expect(m, n, e) for m, n in shapes)
+    assert tm.workspace_bytes([(0, 4)], 2) == 0
+    assert tm.workspace_bytes([(4, 4)], 3) == 0

@@ -1,0 +1,171 @@
+"""Parity of the HIP path (through the C ABI) with the fp64 oracle."""
+import numpy as np
+import pytest
+
+from oracle import turbomuon as O
+from paper_2512_04632_amd import synth
+from gpu_helpers import (BF16_TOL, F32_TOL, EO_RATIO_TOL, from_device, log, make_input, relF,
+                         eo_ratio, to_device)
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+from paper_2512_04632_amd import _lib as tm  # noqa: E402
+
+
+def gpu_orth(Xc, dtype, iters, precond, coeffs=None):
+    t = to_device(Xc, dtype)
+    tm.orthogonalize(t, iters, coeffs, precond)
+    torch.cuda.synchronize()
+    return from_device(t)
+
+
+def tol(dtype):
+    return BF16_TOL if dtype == "bf16" else F32_TOL
+
+
+# ----------------------------------------------------------------- single matrices
+def test_single_256_fp32_aol4():
+    log("case: 256x256 fp32 alpha=1 seed=0 AOL t=4")
+    X = make_input(256, 256, 1.0, 0, "f32")
+    G = gpu_orth(X, "f32", 4, "aol")
+    R = O.orthogonalize(X, 4, None, "aol")
+    e = relF(G, R)
+    log(f"relF={e:.3e} eps_polar gpu={O.eps_polar(G, X):.4f} oracle={O.eps_polar(R, X):.4f}")
+    assert e <= F32_TOL
+
+
+@pytest.mark.parametrize("precond,iters", [("aol", 4), ("frobenius", 5)])
+def test_gpt2_mlp_768x3072_bf16(precond, iters):
+    log(f"case: 768x3072 bf16 alpha=0.8 seed=0 {precond} t={iters}")
+    X = make_input(768, 3072, 0.8, 0, "bf16")
+    G = gpu_orth(X, "bf16", iters, precond)
+    R = O.orthogonalize(X, iters, None, precond)
+    e, r = relF(G, R), eo_ratio(G, R)
+    log(f"relF={e:.3e} eo_ratio={r:.4f}")
+    assert e <= BF16_TOL
+    assert abs(r - 1) <= EO_RATIO_TOL
+
+
+SHAPES = [(1, 1), (1, 8), (8, 1), (5, 3), (17, 33), (33, 17), (64, 64), (100, 300), (300, 100),
+          (129, 130), (64, 576), (257, 520), (520, 257), (96, 1000)]
+
+
+@pytest.mark.parametrize("m,n", SHAPES)
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+@pytest.mark.parametrize("precond,iters", [("aol", 4), ("frobenius", 5), ("aol", 1)])
+def test_shapes(m, n, dtype, precond, iters):
+    log(f"case: {m}x{n} {dtype} {precond} t={iters}")
+    X = make_input(m, n, 0.8, m * 7 + n, dtype)
+    G = gpu_orth(X, dtype, iters, precond)
+    R = O.orthogonalize(X, iters, None, precond)
+    e = relF(G, R)
+    log(f"relF={e:.3e}")
+    assert e <= tol(dtype)
+
+
+@pytest.mark.parametrize("m,n", [(17, 33), (33, 17), (256, 256), (100, 300), (300, 100)])
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+@pytest.mark.parametrize("precond", ["aol", "frobenius"])
+def test_iters0_is_preconditioned_input(m, n, dtype, precond):
+    log(f"case: iters=0 {m}x{n} {dtype} {precond}")
+    X = make_input(m, n, 1.0, 3, dtype)
+    G = gpu_orth(X, dtype, 0, precond)
+    R = O.preconditioned(X, precond)
+    assert relF(G, R) <= (4e-3 if dtype == "bf16" else 1e-6)
+    u = 2.0 ** -8 if dtype == "bf16" else 2.0 ** -24
+    assert np.linalg.norm(G, 2) <= 1 + 4 * u   # AOL / Frobenius bound ||X1||_2 <= 1
+
+
+def test_precond_none_and_iters0_none_is_identity():
+    X = make_input(40, 70, 1.0, 1, "bf16")
+    X = synth.cast(X / np.linalg.norm(X, 2), "bf16")
+    assert np.array_equal(gpu_orth(X, "bf16", 0, "none"), X)
+    G = gpu_orth(X, "bf16", 3, "none")
+    assert relF(G, O.orthogonalize(X, 3, None, "none")) <= BF16_TOL
+
+
+# Coefficient choices that isolate the steps: (1,0,0) keeps X1, (0,1,0) gives
+# X1 X1^T X1 (Gram + update), (0,0,1) gives (X1 X1^T)^2 X1 (Gram, poly, update).
+@pytest.mark.parametrize("coeffs", [[(1.0, 0.0, 0.0)], [(0.0, 1.0, 0.0)], [(0.0, 0.0, 1.0)],
+                                    [(1.5, -0.5, 0.0)] * 3,
+                                    [(4.0848, -6.8946, 2.9270), (3.9505, -6.3029, 2.6377),
+                                     (3.7418, -5.5913, 2.3037), (2.8769, -3.1427, 1.2046)]])
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+@pytest.mark.parametrize("m,n", [(130, 250), (250, 130)])
+def test_step_isolating_coefficients(coeffs, dtype, m, n):
+    log(f"case: coeffs={coeffs[0]}.. {m}x{n} {dtype}")
+    X = make_input(m, n, 0.8, 5, dtype)
+    G = gpu_orth(X, dtype, len(coeffs), "aol", coeffs)
+    R = O.orthogonalize(X, len(coeffs), coeffs, "aol")
+    assert relF(G, R) <= tol(dtype)
+
+
+def test_zero_matrix_and_zero_row():
+    for dtype in ("bf16", "f32"):
+        for pre in ("aol", "frobenius"):
+            Z = np.zeros((48, 80))
+            assert np.all(gpu_orth(Z, dtype, 4, pre) == 0)
+        X = make_input(48, 80, 1.0, 2, dtype)
+        X[7] = 0.0
+        G = gpu_orth(X, dtype, 4, "aol")
+        assert np.all(G[7] == 0) and np.all(np.isfinite(G))
+        assert relF(G, O.orthogonalize(X, 4)) <= tol(dtype)
+
+
+# ----------------------------------------------------------------- batch / group equality
+@pytest.mark.parametrize("m,n", [(96, 200), (200, 96), (256, 256)])
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_batched_grouped_single_are_bitwise_equal(m, n, dtype):
+    log(f"case: batch/group equality {m}x{n} {dtype}")
+    Xs = [make_input(m, n, 0.8, s, dtype) for s in range(3)]
+    single = [gpu_orth(X, dtype, 4, "aol") for X in Xs]
+    tb = torch.stack([to_device(X, dtype) for X in Xs]).contiguous()
+    tm.orthogonalize(tb, 4, None, "aol")
+    tg = [to_device(X, dtype) for X in Xs]
+    tm.orthogonalize_grouped(tg, 4, None, "aol")
+    torch.cuda.synchronize()
+    for i in range(3):
+        assert np.array_equal(from_device(tb[i]), single[i])
+        assert np.array_equal(from_device(tg[i]), single[i])
+    again = gpu_orth(Xs[0], dtype, 4, "aol")
+    assert np.array_equal(again, single[0])        # run-to-run determinism
+
+
+# ----------------------------------------------------------------- grouped workloads
+def run_workload(name, iters=4, precond="aol"):
+    shapes = synth.workload_shapes(name)
+    dtype = synth.WORKLOADS[name]["dtype"]
+    Xs = [make_input(m, n, a, s, dtype) for (m, n, a, s) in shapes]
+    ts = [to_device(X, dtype) for X in Xs]
+    tm.orthogonalize_grouped(ts, iters, None, precond)
+    torch.cuda.synchronize()
+    return Xs, [from_device(t) for t in ts]
+
+
+def test_grouped_gpt2_small_72_matrices():
+    log("case: grouped gpt2_small_12layer (72 matrices)")
+    Xs, Gs = run_workload("gpt2_small_12layer")
+    worst = 0.0
+    for i, (X, G) in enumerate(zip(Xs, Gs)):
+        if i % 6 and i < 48:
+            continue                      # every 6th attention matrix, all MLP matrices
+        R = O.orthogonalize(X, 4)
+        e, r = relF(G, R), eo_ratio(G, R)
+        worst = max(worst, e)
+        assert e <= BF16_TOL and abs(r - 1) <= EO_RATIO_TOL, (i, e, r)
+    log(f"worst relF={worst:.3e}")
+
+
+def test_grouped_resnet_conv_64_matrices():
+    log("case: grouped resnet_conv_64 (64 matrices)")
+    Xs, Gs = run_workload("resnet_conv_64")
+    worst = 0.0
+    for i, (X, G) in enumerate(zip(Xs, Gs)):
+        if i % 4:
+            continue
+        R = O.orthogonalize(X, 4)
+        e, r = relF(G, R), eo_ratio(G, R)
+        worst = max(worst, e)
+        assert e <= BF16_TOL and abs(r - 1) <= EO_RATIO_TOL, (i, e, r)
+    log(f"worst relF={worst:.3e}")
