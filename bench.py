@@ -50,6 +50,10 @@ def main(argv=None) -> int:
     ap.add_argument("--precond", default="aol", choices=["aol", "frobenius", "none"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-check", action="store_true")
+    ap.add_argument("--inputs", default="powerlaw", choices=["powerlaw", "gaussian"],
+                    help="powerlaw: the seeded power-law-plus-noise recipe (QR on the GPU); "
+                         "gaussian: i.i.d. N(0,1) entries, the paper's own synthetic law "
+                         "(for counter runs, where the QR library is not wanted)")
     args = ap.parse_args(argv)
     if args.gpus != 1:
         print(f"bench.py: this build measures one GPU only (asked for --gpus {args.gpus}); "
@@ -73,7 +77,12 @@ def main(argv=None) -> int:
         print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
     progress(f"generating {count} x {m}x{n} {dtype} alpha={alpha}")
-    X = synth.power_law_batch_device(count, m, n, alpha, seed=0, device=dev)
+    if args.inputs == "powerlaw":
+        X = synth.power_law_batch_device(count, m, n, alpha, seed=0, device=dev)
+    else:
+        g = torch.Generator(device=dev)
+        g.manual_seed(0)
+        X = torch.randn((count, m, n), generator=g, device=dev, dtype=torch.float32).to(torch.bfloat16)
     torch.cuda.synchronize()
     x0_host = X[0].float().cpu().numpy().astype(np.float64)   # oracle input (exact bf16 values)
 
@@ -127,7 +136,8 @@ def main(argv=None) -> int:
         "scaling": "weak",
         "vs_baseline": None,
         "dtype": dtype,
-        "data": "synthetic (seeded power-law spectrum + 0.01 Gaussian noise)",
+        "data": ("synthetic (seeded power-law spectrum + 0.01 Gaussian noise)"
+                 if args.inputs == "powerlaw" else "synthetic (seeded i.i.d. N(0,1))"),
         "config": {"workload": args.workload, "matrices": count, "m": m, "n": n,
                    "alpha": alpha, "iters": args.iters, "precond": args.precond},
         "tflops_algorithmic": round(tflops, 2),

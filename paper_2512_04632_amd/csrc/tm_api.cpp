@@ -18,7 +18,8 @@
 #include "turbomuon.h"
 
 namespace tmk {
-hipError_t launch_phase_bf16(int kind, int cfg, const Phase& P, hipStream_t st);
+hipError_t launch_elementwise_bf16(int kind, const Phase& P, hipStream_t st);
+hipError_t launch_fast_bf16(int kind, int cfg, const Phase& P, hipStream_t st);
 hipError_t launch_phase_f32(int kind, int cfg, const Phase& P, hipStream_t st);
 }  // namespace tmk
 
@@ -74,6 +75,7 @@ void collect_timing() {
 struct Item {
   char* x;
   uint32_t k, N;
+  uint32_t kp, Np;     // padded workspace dims (set by the planner)
   uint32_t count;
   bool tall;
 };
@@ -121,16 +123,38 @@ tm_status get_workspace(int dev, hipStream_t st, size_t bytes, char** out) {
 }
 
 uint64_t item_ws(const Item& it, int esz) {
-  return tmk::ws_layout(it.k, it.N, uint32_t(esz)).total * it.count;
+  return tmk::ws_layout(it.kp, it.Np, uint32_t(esz)).total * it.count;
 }
 
-// Pick the largest tile whose launch still spans at least one wave of the
-// chip's 256 compute units; otherwise the smallest tile.
+// Generic (fp32) path: pick per phase the largest tile whose launch still
+// spans one wave of the chip's 256 compute units; otherwise the smallest.
 int choose_cfg(int kind, const std::vector<Item>& items) {
   for (int cfg = 0; cfg < tmk::kNumCfg - 1; ++cfg) {
     uint64_t tiles = 0;
-    for (const Item& it : items) tiles += uint64_t(it.count) * tmk::blocks_per_matrix(kind, cfg, it.k, it.N);
+    for (const Item& it : items)
+      tiles += uint64_t(it.count) * tmk::blocks_per_matrix(kind, cfg, it.k, it.N, it.kp, it.Np);
     if (tiles >= 256) return cfg;
+  }
+  return tmk::kNumCfg - 1;
+}
+
+// bf16 path: one square tile for every phase of the call.  Take the largest
+// tile whose zero padding adds at most 30% to the call's products and whose
+// update still has about two waves of tiles for the 256 compute units.
+int choose_tile_cfg(const std::vector<Item>& items) {
+  double real = 0.0;
+  for (const Item& it : items)
+    real += double(it.count) * (3.0 * it.k * double(it.k) * it.N + double(it.k) * it.k * it.k);
+  for (int cfg = 0; cfg < tmk::kNumCfg - 1; ++cfg) {
+    const uint32_t T = uint32_t(tmk::cfg_tile(cfg));
+    double padded = 0.0, tiles = 0.0;
+    for (const Item& it : items) {
+      uint32_t kp, Np;
+      tmk::tiled_dims(it.k, it.N, T, &kp, &Np);
+      padded += double(it.count) * (3.0 * kp * double(kp) * Np + double(kp) * kp * kp);
+      tiles += double(it.count) * (kp / T) * (Np / T);
+    }
+    if (padded <= 1.3 * real && tiles >= 480.0) return cfg;
   }
   return tmk::kNumCfg - 1;
 }
@@ -159,10 +183,14 @@ tm_status launch(const Plan& pl, int kind, int cfg, int src, int dst, float a, f
       E.ws = pl.ws_off[base + i];
       E.k = it.k;
       E.N = it.N;
+      E.kp = it.kp;
+      E.Np = it.Np;
       E.count = it.count;
       E.flags = it.tall ? tmk::kTall : 0u;
       E.tile_start = uint32_t(start);
-      E.tiles_per = (tall_only && !it.tall) ? 0u : tmk::blocks_per_matrix(kind, cfg, it.k, it.N);
+      E.tiles_per = (tall_only && !it.tall)
+                        ? 0u
+                        : tmk::blocks_per_matrix(kind, cfg, it.k, it.N, it.kp, it.Np);
       start += uint64_t(E.tiles_per) * it.count;
     }
     if (start >= (uint64_t(1) << 31))
@@ -183,8 +211,13 @@ tm_status launch(const Plan& pl, int kind, int cfg, int src, int dst, float a, f
         return fail(TM_ERR_HIP, "hipEventCreate failed");
       (void)hipEventRecord(tl.start, pl.st);
     }
-    const hipError_t e = pl.esz == 2 ? tmk::launch_phase_bf16(kind, cfg, P, pl.st)
-                                     : tmk::launch_phase_f32(kind, cfg, P, pl.st);
+    hipError_t e;
+    if (pl.esz == 4)
+      e = tmk::launch_phase_f32(kind, cfg, P, pl.st);
+    else if (kind == tmk::kKindFrob || kind == tmk::kKindAolVector || kind == tmk::kKindApplyScale)
+      e = tmk::launch_elementwise_bf16(kind, P, pl.st);
+    else
+      e = tmk::launch_fast_bf16(kind, cfg, P, pl.st);
     if (tl.start) {
       (void)hipEventRecord(tl.stop, pl.st);
       g_timed.push_back(tl);
@@ -195,25 +228,52 @@ tm_status launch(const Plan& pl, int kind, int cfg, int src, int dst, float a, f
   return TM_OK;
 }
 
-tm_status run(std::vector<Item>& items, int esz, int iters, const float* coeffs, int precond,
-              hipStream_t st) {
-  if (items.empty()) return TM_OK;
-  std::lock_guard<std::mutex> lock(g_mu);
-  int dev = 0;
-  tm_status s = check_device(&dev);
-  if (s != TM_OK) return s;
-  Plan pl;
-  pl.items = &items;
-  pl.esz = esz;
-  pl.st = st;
-  uint64_t total = 0;
-  for (const Item& it : items) {
-    pl.ws_off.push_back(total);
-    total += item_ws(it, esz);
+// bf16: zero-padded tiled workspace, matrix-core kernels of tm_fast.hip.
+tm_status plan_bf16(const Plan& pl, int iters, const float* coeffs, int precond, int tcfg) {
+  const bool aol = precond == TM_PRECOND_AOL, frob = precond == TM_PRECOND_FROBENIUS;
+  const int T = tmk::cfg_tile(tcfg);
+  tm_status s = TM_OK;
+  if (iters > 0 || aol) s = launch(pl, tmk::kKindLoadIn, 0, 0, 0, 0.f, 0.f, 0.f, 0u, 0, false);
+  if (s == TM_OK && frob) {  // Algorithm 1, first line: s = 1 / ||X0||_F
+    s = launch(pl, tmk::kKindFrob, 0, 0, 0, 0.f, 0.f, 0.f, 0u, 0, false);
+    if (s == TM_OK) s = launch(pl, tmk::kKindAolVector, 0, 0, 0, 0.f, 0.f, 0.f, tmk::kFrob, 0, false);
   }
-  s = get_workspace(dev, st, size_t(total), &pl.ws);
   if (s != TM_OK) return s;
+  if (iters == 0) {
+    if (aol) {
+      s = launch(pl, tmk::kKindGram, tcfg, tmk::kSlotFirst, 0, 0.f, 0.f, 0.f,
+                 tmk::kRowSum | tmk::kA32, 0, false);
+      if (s == TM_OK) s = launch(pl, tmk::kKindAolVector, 0, 0, 0, 0.f, 0.f, 0.f, 0u, T, false);
+      if (s != TM_OK) return s;
+    }
+    if (aol || frob) s = launch(pl, tmk::kKindApplyScale, 0, 0, 0, 0.f, 0.f, 0.f, 0u, 0, false);
+    return s;
+  }
+  int src = tmk::kSlotFirst;
+  for (int it = 1; it <= iters && s == TM_OK; ++it) {
+    const float a = coeffs ? coeffs[3 * (it - 1)] : kA;
+    const float b = coeffs ? coeffs[3 * (it - 1) + 1] : kB;
+    const float c = coeffs ? coeffs[3 * (it - 1) + 2] : kC;
+    const int dst = it == iters ? tmk::kSlotFinal : (it % 2 == 1 ? tmk::kSlotAlt1 : tmk::kSlotAlt2);
+    const bool first = it == 1;
+    const uint32_t scale = (first && (aol || frob)) ? tmk::kScale : 0u;
+    const uint32_t gflags = ((first && aol) ? tmk::kRowSum : 0u) | (scale ? tmk::kA32 : 0u);
+    s = launch(pl, tmk::kKindGram, tcfg, src, 0, 0.f, 0.f, 0.f, gflags, 0, false);
+    if (s == TM_OK && first && aol)  // Algorithm 2, second line: the AOL vector
+      s = launch(pl, tmk::kKindAolVector, 0, 0, 0, 0.f, 0.f, 0.f, 0u, T, false);
+    if (s == TM_OK && scale)         // A1 = diag(s) A0 diag(s), one rounding
+      s = launch(pl, tmk::kKindScaleA, 0, 0, 0, 0.f, 0.f, 0.f, 0u, 0, false);
+    if (s == TM_OK) s = launch(pl, tmk::kKindPoly, tcfg, 0, 0, a, b, c, scale, 0, false);
+    if (s == TM_OK) s = launch(pl, tmk::kKindUpdate, tcfg, src, dst, a, b, c, scale, 0, false);
+    src = dst;
+  }
+  return s;
+}
 
+// fp32: generic kernels of tm_kernels.hip.
+tm_status plan_f32(const Plan& pl, int iters, const float* coeffs, int precond) {
+  const std::vector<Item>& items = *pl.items;
+  tm_status s = TM_OK;
   bool any_tall = false;
   for (const Item& it : items) any_tall = any_tall || it.tall;
   if (any_tall && (iters > 0 || precond == TM_PRECOND_AOL)) {
@@ -266,6 +326,34 @@ tm_status run(std::vector<Item>& items, int esz, int iters, const float* coeffs,
   return s;
 }
 
+tm_status run(std::vector<Item>& items, int esz, int iters, const float* coeffs, int precond,
+              hipStream_t st) {
+  if (items.empty()) return TM_OK;
+  std::lock_guard<std::mutex> lock(g_mu);
+  int dev = 0;
+  tm_status s = check_device(&dev);
+  if (s != TM_OK) return s;
+  int tcfg = 0;
+  if (esz == 2) {
+    tcfg = choose_tile_cfg(items);
+    for (Item& it : items) tmk::tiled_dims(it.k, it.N, uint32_t(tmk::cfg_tile(tcfg)), &it.kp, &it.Np);
+  } else {
+    for (Item& it : items) tmk::generic_dims(it.k, it.N, &it.kp, &it.Np);
+  }
+  Plan pl;
+  pl.items = &items;
+  pl.esz = esz;
+  pl.st = st;
+  uint64_t total = 0;
+  for (const Item& it : items) {
+    pl.ws_off.push_back(total);
+    total += item_ws(it, esz);
+  }
+  s = get_workspace(dev, st, size_t(total), &pl.ws);
+  if (s != TM_OK) return s;
+  return esz == 2 ? plan_bf16(pl, iters, coeffs, precond, tcfg) : plan_f32(pl, iters, coeffs, precond);
+}
+
 tm_status check_common(int iters, const float* coeffs, int precond) {
   if (iters < 0 || iters > TM_MAX_ITERS)
     return fail(TM_ERR_INVALID_ARG, "iters out of range [0, " + std::to_string(TM_MAX_ITERS) + "]");
@@ -288,6 +376,8 @@ Item make_item(void* X, int64_t m, int64_t n, int64_t count) {
   it.tall = m > n;
   it.k = uint32_t(std::min(m, n));
   it.N = uint32_t(std::max(m, n));
+  it.kp = it.k;
+  it.Np = it.N;
   it.count = uint32_t(count);
   return it;
 }
@@ -359,10 +449,18 @@ tm_status tm_orthogonalize_grouped_f32(float* const* X, const int64_t* m, const 
 
 uint64_t tm_workspace_bytes(const int64_t* m, const int64_t* n, int64_t count, int dtype_bytes) {
   if (m == nullptr || n == nullptr || count < 0 || (dtype_bytes != 2 && dtype_bytes != 4)) return 0;
-  uint64_t total = 0;
+  std::vector<Item> items;
   for (int64_t g = 0; g < count; ++g) {
     if (m[g] < 1 || n[g] < 1 || m[g] > TM_MAX_DIM || n[g] > TM_MAX_DIM) return 0;
-    total += item_ws(make_item(nullptr, m[g], n[g], 1), dtype_bytes);
+    items.push_back(make_item(nullptr, m[g], n[g], 1));
+  }
+  if (items.empty()) return 0;
+  const int tcfg = dtype_bytes == 2 ? choose_tile_cfg(items) : 0;
+  uint64_t total = 0;
+  for (Item& it : items) {
+    if (dtype_bytes == 2) tmk::tiled_dims(it.k, it.N, uint32_t(tmk::cfg_tile(tcfg)), &it.kp, &it.Np);
+    else tmk::generic_dims(it.k, it.N, &it.kp, &it.Np);
+    total += item_ws(it, dtype_bytes);
   }
   return total;
 }

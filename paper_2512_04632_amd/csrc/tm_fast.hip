@@ -1,0 +1,571 @@
+// bf16 matrix-core path of the Turbo-Muon orthogonalizer for gfx950 (MI355X).
+//
+// Every matrix is held in a zero-padded workspace copy whose dims are
+// multiples of the square tile T (256, 128 or 64), so every tile is full: the
+// main loops carry no bounds checks and zero padding is preserved by the
+// iteration (padded rows and columns of Y, A and B stay zero).
+//
+// Phases (one launch each over the tiles of all matrices of a call):
+//   k_load_in     W1 = X (wide) or X^T (tall), zero padded
+//   k_gram_fast   A = Y Y^T, upper tiles, mirrored bf16 store; at iteration 1
+//                 the fp32 accumulators are stored instead (A0 is rescaled
+//                 before rounding) and the epilogue emits the AOL row sums
+//                 sum_j |A0_ij| (eq. (aol))
+//   k_scale_a     A1 = diag(s) A0 diag(s), rounded once to bf16
+//   k_poly_fast   B~ = b A + c A A + a I, upper tiles, mirrored store; at
+//                 iteration 1 the stored matrix is B~ diag(s), which applies
+//                 X1 = diag(s) X0 inside the next product
+//   k_update_fast Y' = B~ Y = a Y + B Y: the axpy of the update rides on B~'s
+//                 diagonal, so the update is a single product with no second
+//                 read of Y
+//
+// Main loop: 256 threads = 4 wave64s in a 2 x 2 grid, each owning a
+// (T/2) x (T/2) block of 32 x 32 v_mfma_f32_32x32x16_bf16 accumulators.  K
+// advances 32 elements per stage through a 4-stage LDS ring filled by
+// global_load_lds_dwordx4 (direct to LDS, no VGPR staging), three stages in
+// flight.  K-contiguous operands are stored as 64-byte rows with the 16-byte
+// chunk index XOR ((row / 4) % 4); the update's Y operand is staged in its
+// row-major layout (32 rows of T bf16) with 32-byte chunks XOR-swizzled per
+// row and read with ds_read_b64_tr_b16, which hands each lane 4 consecutive
+// K values of one column.  Both layouts are free of LDS bank conflicts for
+// the reads.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "tm_internal.h"
+
+namespace tmk {
+namespace fast {
+
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef float f32x16_t __attribute__((ext_vector_type(16)));
+typedef short s16x4_t __attribute__((ext_vector_type(4)));
+
+constexpr int BK = 32;        // K elements per stage (64 bytes of a K-contiguous row)
+constexpr int STAGES = 4;
+
+template <int T>
+struct Tile {
+  static constexpr int TW = T / 2;              // wave tile
+  static constexpr int F = TW / 32;             // 32 x 32 blocks per wave side
+  static constexpr int A_BYTES = T * BK * 2;    // one operand stage
+  static constexpr int STAGE = 2 * A_BYTES;
+  static constexpr int LDS = STAGES * STAGE;
+  static constexpr int PER_STAGE = T / 32;      // DMA instructions per wave per stage
+};
+
+__device__ inline float bf2f(uint16_t v) { return __uint_as_float(uint32_t(v) << 16); }
+__device__ inline uint16_t f2bf(float f) {     // v_cvt_pk_bf16_f32: round to nearest even
+  __bf16 h = static_cast<__bf16>(f);
+  return __builtin_bit_cast(uint16_t, h);
+}
+
+__device__ inline uint32_t lds_addr(const void* p) {
+  return static_cast<uint32_t>(reinterpret_cast<uintptr_t>(p));
+}
+
+// One 16-byte-per-lane direct global -> LDS load: lane i writes LDS bytes
+// [lds + 16 i, lds + 16 i + 16).  Issued through inline assembly so that the
+// compiler does not serialise the LDS reads of other stages behind it; the
+// ring's own s_waitcnt/s_barrier pairs order it.
+__device__ inline void dma16(const void* base, uint32_t voff, uint32_t lds) {
+  asm volatile(
+      "s_mov_b32 m0, %2\n\t"
+      "s_nop 0\n\t"
+      "global_load_lds_dwordx4 %0, %1\n"
+      :
+      : "v"(voff), "s"(base), "s"(lds)
+      : "memory", "m0");
+}
+
+// Wait until at most `pending` DMA instructions of this wave are in flight and
+// all of its LDS reads are done, then join the workgroup barrier.
+template <int PENDING>
+__device__ inline void ring_sync() {
+  if constexpr (PENDING == 0) asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory");
+  else if constexpr (PENDING == 2) asm volatile("s_waitcnt vmcnt(2) lgkmcnt(0)\n\ts_barrier" ::: "memory");
+  else if constexpr (PENDING == 4) asm volatile("s_waitcnt vmcnt(4) lgkmcnt(0)\n\ts_barrier" ::: "memory");
+  else if constexpr (PENDING == 8) asm volatile("s_waitcnt vmcnt(8) lgkmcnt(0)\n\ts_barrier" ::: "memory");
+  else if constexpr (PENDING == 16) asm volatile("s_waitcnt vmcnt(16) lgkmcnt(0)\n\ts_barrier" ::: "memory");
+  else static_assert(PENDING == 0, "unsupported in-flight count");
+}
+
+// ---------------------------------------------------------------- DMA issue
+// K-contiguous operand: T rows x 32 bf16 (64 bytes).  Logical 16-byte chunk c
+// of row r lives at chunk c ^ ((r >> 2) & 3).  One instruction fills 16 rows.
+template <int T>
+__device__ inline void issue_kc(const uint16_t* src, int64_t ld, int k0, uint32_t lds) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+#pragma unroll
+  for (int q = 0; q < T / 64; ++q) {
+    const int j = wave + 4 * q;
+    const int r = j * 16 + (lane >> 2);
+    const int c = (lane & 3) ^ ((r >> 2) & 3);
+    const uint32_t voff = uint32_t((int64_t(r) * ld + k0 + c * 8) * 2);
+    dma16(src, voff, __builtin_amdgcn_readfirstlane(lds + uint32_t(j) * 1024u));
+  }
+}
+
+// 32-byte chunk swizzle of the row-major Y stage (row = 2T bytes).
+template <int T>
+__device__ inline int swz_y(int r) {
+  return T >= 128 ? 2 * (r & 3) : 2 * ((r >> 1) & 1);
+}
+
+// Row-major operand (the update's Y): 32 rows (K) x T columns, row = 2T bytes.
+template <int T>
+__device__ inline void issue_rm(const uint16_t* src, int64_t ld, int k0, uint32_t lds) {
+  constexpr int ROWB = 2 * T;
+  constexpr int LPR = ROWB / 16;          // lanes per row
+  constexpr int RPI = 1024 / ROWB;        // rows per instruction
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+#pragma unroll
+  for (int q = 0; q < T / 64; ++q) {
+    const int j = wave + 4 * q;
+    const int r = j * RPI + lane / LPR;
+    const int p16 = lane % LPR;
+    const int c = (p16 >> 1) ^ swz_y<T>(r);
+    const uint32_t voff = uint32_t((int64_t(k0 + r) * ld + c * 16 + (p16 & 1) * 8) * 2);
+    dma16(src, voff, __builtin_amdgcn_readfirstlane(lds + uint32_t(j) * 1024u));
+  }
+}
+
+// ---------------------------------------------------------------- compute
+template <int T, bool RM>
+__device__ inline void compute_stage(f32x16_t (&acc)[Tile<T>::F][Tile<T>::F], const char* sa,
+                                     const char* sb, int wm, int wn) {
+  constexpr int F = Tile<T>::F, TW = Tile<T>::TW;
+  const int lane = threadIdx.x & 63;
+  const int lr = lane & 31, lh = lane >> 5;
+#pragma unroll
+  for (int kk = 0; kk < BK / 16; ++kk) {
+    uint4 a[F], b[F];
+    const int c = 2 * kk + lh;
+#pragma unroll
+    for (int f = 0; f < F; ++f) {
+      const int r = wm * TW + f * 32 + lr;
+      a[f] = *reinterpret_cast<const uint4*>(sa + r * 64 + 16 * (c ^ ((r >> 2) & 3)));
+    }
+    if constexpr (!RM) {
+#pragma unroll
+      for (int f = 0; f < F; ++f) {
+        const int r = wn * TW + f * 32 + lr;
+        b[f] = *reinterpret_cast<const uint4*>(sb + r * 64 + 16 * (c ^ ((r >> 2) & 3)));
+      }
+    } else {
+      // Lane q of 16-lane group g addresses row kb + q/4, columns n + 4(q%4);
+      // the transposed read returns rows kb..kb+3 of column n + q.
+      const int g = lane >> 4, q = lane & 15;
+      const int kb = 16 * kk + 8 * (g >> 1) + (q >> 2);
+#pragma unroll
+      for (int f = 0; f < F; ++f) {
+        const int chunk = (wn * TW + f * 32) / 16 + (g & 1);
+        s16x4_t v[2];
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+          const int row = kb + 4 * h;
+          const char* p = sb + row * (2 * T) + 32 * (chunk ^ swz_y<T>(row)) + 8 * (q & 3);
+          v[h] = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+              (__attribute__((address_space(3))) s16x4_t*)(lds_addr(p)));
+        }
+        b[f] = __builtin_bit_cast(uint4, v);
+      }
+    }
+#pragma unroll
+    for (int fm = 0; fm < F; ++fm)
+#pragma unroll
+      for (int fn = 0; fn < F; ++fn)
+        acc[fm][fn] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+            __builtin_bit_cast(bf16x8_t, a[fm]), __builtin_bit_cast(bf16x8_t, b[fn]), acc[fm][fn],
+            0, 0, 0);
+  }
+}
+
+// acc = A (T x K, K-contiguous rows of a) * B^T where B's rows are the
+// K-contiguous rows of b (RM = false) or B = the K x T row-major block of b
+// (RM = true).  K is a multiple of BK; every tile is full.
+template <int T, bool RM>
+__device__ inline void mainloop(f32x16_t (&acc)[Tile<T>::F][Tile<T>::F], char* smem,
+                                const uint16_t* a, int64_t lda, const uint16_t* b, int64_t ldb,
+                                int K) {
+  constexpr int F = Tile<T>::F, PS = Tile<T>::PER_STAGE;
+  const int wave = threadIdx.x >> 6;
+  const int wm = wave >> 1, wn = wave & 1;
+#pragma unroll
+  for (int fm = 0; fm < F; ++fm)
+#pragma unroll
+    for (int fn = 0; fn < F; ++fn)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) acc[fm][fn][v] = 0.f;
+
+  const uint32_t lds0 = lds_addr(smem);
+  const int nk = K / BK;
+  auto issue = [&](int kt) {
+    const uint32_t st = lds0 + uint32_t((kt % STAGES) * Tile<T>::STAGE);
+    issue_kc<T>(a, lda, kt * BK, st);
+    if constexpr (RM) issue_rm<T>(b, ldb, kt * BK, st + Tile<T>::A_BYTES);
+    else issue_kc<T>(b, ldb, kt * BK, st + Tile<T>::A_BYTES);
+  };
+#pragma unroll
+  for (int s = 0; s < STAGES - 1; ++s)
+    if (s < nk) issue(s);
+
+  for (int kt = 0; kt < nk; ++kt) {
+    // stages kt+1 .. kt+2 may stay in flight
+    const int ahead = min(nk - 1, kt + STAGES - 2) - kt;
+    if (ahead >= 2) ring_sync<2 * PS>();
+    else if (ahead == 1) ring_sync<PS>();
+    else ring_sync<0>();
+    if (kt + STAGES - 1 < nk) issue(kt + STAGES - 1);
+    const char* st = smem + (kt % STAGES) * Tile<T>::STAGE;
+    compute_stage<T, RM>(acc, st, st + Tile<T>::A_BYTES, wm, wn);
+  }
+  ring_sync<0>();   // the ring is free for the epilogue
+}
+
+// ---------------------------------------------------------------- mapping
+__device__ inline int xcd_remap(int p, int total) {
+  const int q = total >> 3, r = total & 7;
+  const int x = p & 7, j = p >> 3;
+  return x * q + min(x, r) + j;
+}
+
+struct Loc {
+  int ent, mat, tile;
+};
+
+__device__ inline Loc locate(const Phase& P, int lid) {
+  int e = 0;
+  while (e + 1 < P.nent && lid >= int(P.e[e + 1].tile_start)) ++e;
+  const int r = lid - int(P.e[e].tile_start);
+  const int per = int(P.e[e].tiles_per);
+  Loc L;
+  L.ent = e;
+  L.mat = r / per;
+  L.tile = r - L.mat * per;
+  return L;
+}
+
+__device__ inline char* ws_of(const Phase& P, const Entry& E, int mat) {
+  return P.ws + E.ws + uint64_t(mat) * ws_layout(E.kp, E.Np, 2).total;
+}
+
+__device__ inline uint16_t* user_of(const Entry& E, int mat) {
+  return reinterpret_cast<uint16_t*>(E.x + uint64_t(mat) * E.k * E.N * 2u);
+}
+
+// Workspace Y buffer of a slot (kp x Np, ld Np): the first slot is W1, then
+// W2, W1, ... (the final slot is the caller's matrix, handled by the update).
+__device__ inline uint16_t* wbuf(const Phase& P, const Entry& E, int mat, int slot) {
+  const WsLayout L = ws_layout(E.kp, E.Np, 2);
+  const bool w1 = slot == kSlotFirst || slot == kSlotAlt2;
+  return reinterpret_cast<uint16_t*>(ws_of(P, E, mat) + (w1 ? L.w1 : L.w2));
+}
+
+__device__ inline void tri_tile(int t, int nb, int& I, int& J) {
+  I = 0;
+  while (t >= nb - I) {
+    t -= nb - I;
+    ++I;
+  }
+  J = I + t;
+}
+
+template <int T>
+__device__ inline int acc_row(int wm, int fm, int v) {
+  return wm * Tile<T>::TW + fm * 32 + 8 * (v >> 2) + 4 * ((threadIdx.x & 63) >> 5) + (v & 3);
+}
+template <int T>
+__device__ inline int acc_col(int wn, int fn) {
+  return wn * Tile<T>::TW + fn * 32 + (threadIdx.x & 31);
+}
+
+// Store tile (I, J) of a symmetric kp x kp matrix (ld kp) and, off the
+// diagonal, its transpose at (J, I).  f gives the value stored at (i, j), g the
+// one stored at the mirrored (j, i).
+template <int T, typename OUT, class Fv, class Gv>
+__device__ inline void store_sym(const f32x16_t (&acc)[Tile<T>::F][Tile<T>::F], OUT* D, int64_t ld,
+                                 int I, int J, Fv f, Gv g) {
+  constexpr int F = Tile<T>::F;
+  const int wave = threadIdx.x >> 6;
+  const int wm = wave >> 1, wn = wave & 1;
+#pragma unroll
+  for (int fm = 0; fm < F; ++fm)
+#pragma unroll
+    for (int fn = 0; fn < F; ++fn) {
+      const int j = J * T + acc_col<T>(wn, fn);
+#pragma unroll
+      for (int v4 = 0; v4 < 4; ++v4) {
+        const int ib = I * T + acc_row<T>(wm, fm, 4 * v4);
+        OUT o[4], m[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          const float x = acc[fm][fn][4 * v4 + u];
+          if constexpr (sizeof(OUT) == 2) {
+            o[u] = f2bf(f(ib + u, j, x));
+            m[u] = f2bf(g(ib + u, j, x));
+          } else {
+            o[u] = f(ib + u, j, x);
+            m[u] = g(ib + u, j, x);
+          }
+        }
+#pragma unroll
+        for (int u = 0; u < 4; ++u) D[int64_t(ib + u) * ld + j] = o[u];
+        if (I != J) {
+          if constexpr (sizeof(OUT) == 2) *reinterpret_cast<uint2*>(D + int64_t(j) * ld + ib) = *reinterpret_cast<uint2*>(m);
+          else *reinterpret_cast<uint4*>(D + int64_t(j) * ld + ib) = *reinterpret_cast<uint4*>(m);
+        }
+      }
+    }
+}
+
+// ---------------------------------------------------------------- kernels
+template <int T>
+__global__ __launch_bounds__(256) void k_gram_fast(const Phase P) {
+  __shared__ __attribute__((aligned(1024))) char smem[Tile<T>::LDS];
+  constexpr int F = Tile<T>::F;
+  const Loc L = locate(P, xcd_remap(blockIdx.x, P.total));
+  const Entry& E = P.e[L.ent];
+  const int kp = int(E.kp), Np = int(E.Np);
+  int I, J;
+  tri_tile(L.tile, kp / T, I, J);
+  const uint16_t* Y = wbuf(P, E, L.mat, P.src);
+  f32x16_t acc[F][F];
+  mainloop<T, false>(acc, smem, Y + int64_t(I) * T * Np, Np, Y + int64_t(J) * T * Np, Np, Np);
+
+  char* w = ws_of(P, E, L.mat);
+  const WsLayout WL = ws_layout(E.kp, E.Np, 2);
+  auto ident = [](int, int, float x) { return x; };
+  if (P.flags & kA32)
+    store_sym<T, float>(acc, reinterpret_cast<float*>(w + WL.a32), kp, I, J, ident, ident);
+  else
+    store_sym<T, uint16_t>(acc, reinterpret_cast<uint16_t*>(w + WL.a), kp, I, J, ident, ident);
+
+  if (P.flags & kRowSum) {
+    // part[Jb][i] = sum over column block Jb of |A0_ij|, from the fp32 accumulators
+    float* part = reinterpret_cast<float*>(w + WL.part);
+    float* rs = reinterpret_cast<float*>(smem);       // [2][T] row sums per wn
+    float* cs = rs + 2 * T;                           // [2][T] column sums per wm
+    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+    const int wm = wave >> 1, wn = wave & 1;
+#pragma unroll
+    for (int fm = 0; fm < F; ++fm)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        float x = 0.f;
+#pragma unroll
+        for (int fn = 0; fn < F; ++fn) x += fabsf(acc[fm][fn][v]);
+#pragma unroll
+        for (int off = 16; off >= 1; off >>= 1) x += __shfl_xor(x, off, 64);
+        if ((lane & 31) == 0) rs[wn * T + acc_row<T>(wm, fm, v)] = x;
+      }
+#pragma unroll
+    for (int fn = 0; fn < F; ++fn) {
+      float x = 0.f;
+#pragma unroll
+      for (int fm = 0; fm < F; ++fm)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) x += fabsf(acc[fm][fn][v]);
+      x += __shfl_xor(x, 32, 64);
+      if (lane < 32) cs[wm * T + acc_col<T>(wn, fn)] = x;
+    }
+    __syncthreads();
+    for (int r = threadIdx.x; r < T; r += 256) {
+      part[int64_t(J) * kp + I * T + r] = rs[r] + rs[T + r];
+      if (I != J) part[int64_t(I) * kp + J * T + r] = cs[r] + cs[T + r];
+    }
+  }
+}
+
+// B~ = b A + c A A + a I (upper tiles, mirrored).  SCALE: A1 = diag(s) A0 diag(s)
+// comes in rounded in A (k_scale_a) and unrounded in a32; the stored matrix
+// is B~1 diag(s).
+template <int T, bool SCALE>
+__global__ __launch_bounds__(256) void k_poly_fast(const Phase P) {
+  __shared__ __attribute__((aligned(1024))) char smem[Tile<T>::LDS];
+  constexpr int F = Tile<T>::F;
+  const Loc L = locate(P, xcd_remap(blockIdx.x, P.total));
+  const Entry& E = P.e[L.ent];
+  const int kp = int(E.kp);
+  int I, J;
+  tri_tile(L.tile, kp / T, I, J);
+  char* w = ws_of(P, E, L.mat);
+  const WsLayout WL = ws_layout(E.kp, E.Np, 2);
+  const uint16_t* A = reinterpret_cast<const uint16_t*>(w + WL.a);
+  uint16_t* B = reinterpret_cast<uint16_t*>(w + WL.b);
+  f32x16_t acc[F][F];
+  mainloop<T, false>(acc, smem, A + int64_t(I) * T * kp, kp, A + int64_t(J) * T * kp, kp, kp);
+  const float a = P.a, b = P.b, c = P.c;
+  if constexpr (SCALE) {
+    const float* A0 = reinterpret_cast<const float*>(w + WL.a32);
+    const float* s = reinterpret_cast<const float*>(w + WL.s);
+    auto val = [=](int i, int j, float x) {
+      const float a1 = A0[int64_t(i) * kp + j] * (s[i] * s[j]);
+      return b * a1 + c * x + (i == j ? a : 0.f);
+    };
+    auto f = [=](int i, int j, float x) { return val(i, j, x) * s[j]; };
+    auto g = [=](int i, int j, float x) { return val(i, j, x) * s[i]; };
+    store_sym<T, uint16_t>(acc, B, kp, I, J, f, g);
+  } else {
+    auto f = [=](int i, int j, float x) {
+      return b * bf2f(A[int64_t(i) * kp + j]) + c * x + (i == j ? a : 0.f);
+    };
+    store_sym<T, uint16_t>(acc, B, kp, I, J, f, f);
+  }
+}
+
+// Y' = B~ Y.  dst = kSlotFinal writes the caller's matrix (tall: transposed),
+// otherwise the workspace slot (whole padded tile).
+template <int T>
+__global__ __launch_bounds__(256) void k_update_fast(const Phase P) {
+  __shared__ __attribute__((aligned(1024))) char smem[Tile<T>::LDS];
+  constexpr int F = Tile<T>::F;
+  const Loc L = locate(P, xcd_remap(blockIdx.x, P.total));
+  const Entry& E = P.e[L.ent];
+  const int kp = int(E.kp), Np = int(E.Np), k = int(E.k), N = int(E.N);
+  // groups of 4 block rows: concurrently running tiles share rows of B~
+  const int nI = kp / T, nL = Np / T;
+  constexpr int GM = 4;
+  const int grp = L.tile / (GM * nL);
+  const int first = grp * GM;
+  const int gsz = min(nI - first, GM);
+  const int rem = L.tile - grp * GM * nL;
+  const int I = first + rem % gsz;
+  const int Lb = rem / gsz;
+
+  char* w = ws_of(P, E, L.mat);
+  const WsLayout WL = ws_layout(E.kp, E.Np, 2);
+  const uint16_t* B = reinterpret_cast<const uint16_t*>(w + WL.b);
+  const uint16_t* Y = wbuf(P, E, L.mat, P.src);
+  f32x16_t acc[F][F];
+  mainloop<T, true>(acc, smem, B + int64_t(I) * T * kp, kp, Y + int64_t(Lb) * T, Np, kp);
+
+  const int wave = threadIdx.x >> 6;
+  const int wm = wave >> 1, wn = wave & 1;
+  if (P.dst != kSlotFinal) {
+    uint16_t* D = wbuf(P, E, L.mat, P.dst);
+#pragma unroll
+    for (int fm = 0; fm < F; ++fm)
+#pragma unroll
+      for (int fn = 0; fn < F; ++fn) {
+        const int l = Lb * T + acc_col<T>(wn, fn);
+#pragma unroll
+        for (int v = 0; v < 16; ++v)
+          D[int64_t(I * T + acc_row<T>(wm, fm, v)) * Np + l] = f2bf(acc[fm][fn][v]);
+      }
+  } else if ((E.flags & kTall) == 0u) {
+    uint16_t* D = user_of(E, L.mat);
+#pragma unroll
+    for (int fm = 0; fm < F; ++fm)
+#pragma unroll
+      for (int fn = 0; fn < F; ++fn) {
+        const int l = Lb * T + acc_col<T>(wn, fn);
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+          const int i = I * T + acc_row<T>(wm, fm, v);
+          if (i < k && l < N) D[int64_t(i) * N + l] = f2bf(acc[fm][fn][v]);
+        }
+      }
+  } else {
+    uint16_t* D = user_of(E, L.mat);   // N x k: element (i, l) of the wide view at l * k + i
+#pragma unroll
+    for (int fm = 0; fm < F; ++fm)
+#pragma unroll
+      for (int fn = 0; fn < F; ++fn) {
+        const int l = Lb * T + acc_col<T>(wn, fn);
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+          const int i = I * T + acc_row<T>(wm, fm, v);
+          if (i < k && l < N) D[int64_t(l) * k + i] = f2bf(acc[fm][fn][v]);
+        }
+      }
+  }
+}
+
+// W1 = X (wide) or X^T (tall) in the padded layout, zeros outside the matrix.
+__global__ __launch_bounds__(256) void k_load_in(const Phase P) {
+  __shared__ uint16_t tile[kTransposeTile][kTransposeTile + 2];
+  const Loc L = locate(P, blockIdx.x);
+  const Entry& E = P.e[L.ent];
+  const int k = int(E.k), N = int(E.N), Np = int(E.Np);
+  const int nI = int(E.kp) / kTransposeTile;
+  const int ti = L.tile % nI, tl = L.tile / nI;
+  const uint16_t* X = user_of(E, L.mat);
+  uint16_t* W = wbuf(P, E, L.mat, kSlotFirst);
+  const bool tall = (E.flags & kTall) != 0u;
+  const int c = threadIdx.x & 63, r0 = threadIdx.x >> 6;
+  if (tall) {
+    for (int r = r0; r < kTransposeTile; r += 4) {
+      const int l = tl * kTransposeTile + r, i = ti * kTransposeTile + c;
+      tile[r][c] = (l < N && i < k) ? X[int64_t(l) * k + i] : uint16_t(0);
+    }
+    __syncthreads();
+    for (int r = r0; r < kTransposeTile; r += 4) {
+      const int i = ti * kTransposeTile + r, l = tl * kTransposeTile + c;
+      W[int64_t(i) * Np + l] = tile[c][r];
+    }
+  } else {
+    for (int r = r0; r < kTransposeTile; r += 4) {
+      const int i = ti * kTransposeTile + r, l = tl * kTransposeTile + c;
+      W[int64_t(i) * Np + l] = (i < k && l < N) ? X[int64_t(i) * N + l] : uint16_t(0);
+    }
+  }
+}
+
+// A = bf16(s_i A0_ij s_j) over the padded kp x kp square; 8 elements per thread.
+__global__ __launch_bounds__(256) void k_scale_a(const Phase P) {
+  const Loc L = locate(P, blockIdx.x);
+  const Entry& E = P.e[L.ent];
+  const int64_t kp = E.kp;
+  char* w = ws_of(P, E, L.mat);
+  const WsLayout WL = ws_layout(E.kp, E.Np, 2);
+  const float* A0 = reinterpret_cast<const float*>(w + WL.a32);
+  const float* s = reinterpret_cast<const float*>(w + WL.s);
+  uint16_t* A = reinterpret_cast<uint16_t*>(w + WL.a);
+  const int64_t idx = int64_t(L.tile) * kElemBlock + int64_t(threadIdx.x) * 8;
+  if (idx >= kp * kp) return;
+  const int64_t i = idx / kp, j = idx - i * kp;   // kp % 8 == 0: the 8 stay in row i
+  const float si = s[i];
+  uint16_t o[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) o[e] = f2bf(A0[idx + e] * (si * s[j + e]));
+  *reinterpret_cast<uint4*>(A + idx) = *reinterpret_cast<const uint4*>(o);
+}
+
+#define TM_LAUNCH(kern) \
+  do { hipLaunchKernelGGL(kern, dim3(P.total), dim3(256), 0, st, P); return hipGetLastError(); } while (0)
+
+template <int T>
+static hipError_t launch_t(int kind, const Phase& P, hipStream_t st) {
+  const bool scale = (P.flags & kScale) != 0u;
+  switch (kind) {
+    case kKindGram: TM_LAUNCH(k_gram_fast<T>);
+    case kKindPoly:
+      if (scale) TM_LAUNCH((k_poly_fast<T, true>));
+      TM_LAUNCH((k_poly_fast<T, false>));
+    case kKindUpdate: TM_LAUNCH(k_update_fast<T>);
+  }
+  return hipErrorInvalidValue;
+}
+
+}  // namespace fast
+
+hipError_t launch_fast_bf16(int kind, int cfg, const Phase& P, hipStream_t st) {
+  if (P.total <= 0) return hipSuccess;
+  if (kind == kKindLoadIn) {
+    hipLaunchKernelGGL(fast::k_load_in, dim3(P.total), dim3(256), 0, st, P);
+    return hipGetLastError();
+  }
+  if (kind == kKindScaleA) {
+    hipLaunchKernelGGL(fast::k_scale_a, dim3(P.total), dim3(256), 0, st, P);
+    return hipGetLastError();
+  }
+  switch (cfg_tile(cfg)) {
+    case 256: return fast::launch_t<256>(kind, P, st);
+    case 128: return fast::launch_t<128>(kind, P, st);
+    case 64: return fast::launch_t<64>(kind, P, st);
+  }
+  return hipErrorInvalidValue;
+}
+
+}  // namespace tmk

@@ -51,6 +51,7 @@ struct Entry {
   char* x;             // user matrix of element 0
   uint64_t ws;         // byte offset of element 0's workspace region
   uint32_t k, N;       // wide view: k = min(m, n) rows, N = max(m, n) columns
+  uint32_t kp, Np;     // padded workspace dims: rows of Y, A, B and ld of A, B (kp); ld of Y (Np)
   uint32_t count;      // matrices in this entry
   uint32_t flags;      // kTall
   uint32_t tile_start; // first logical block of this entry in the launch
@@ -74,23 +75,27 @@ TM_HD int cfg_tile(int cfg) { return cfg == 0 ? 256 : (cfg == 1 ? 128 : 64); }
 
 // Logical blocks per matrix of each kernel.
 enum Kind { kKindTransposeIn, kKindFrob, kKindGram, kKindAolVector, kKindPoly,
-            kKindUpdate, kKindApplyScale, kKindCopyOut };
+            kKindUpdate, kKindApplyScale, kKindCopyOut, kKindLoadIn, kKindScaleA };
 constexpr int kTransposeTile = 64;
 constexpr int kElemBlock = 2048;     // elements per block of the elementwise kernels
 
 TM_HD uint32_t tri(uint32_t nb) { return nb * (nb + 1u) / 2u; }
 
-TM_HD uint32_t blocks_per_matrix(int kind, int cfg, uint32_t k, uint32_t N) {
+// k, N: wide-view dims; kp, Np: padded workspace dims.
+TM_HD uint32_t blocks_per_matrix(int kind, int cfg, uint32_t k, uint32_t N, uint32_t kp,
+                                 uint32_t Np) {
   const uint32_t T = uint32_t(cfg_tile(cfg));
   switch (kind) {
     case kKindTransposeIn: return cdiv(k, kTransposeTile) * cdiv(N, kTransposeTile);
+    case kKindLoadIn: return cdiv(kp, kTransposeTile) * cdiv(Np, kTransposeTile);
     case kKindFrob: return uint32_t(kFrobBlocks);
     case kKindGram:
-    case kKindPoly: return tri(cdiv(k, T));
-    case kKindAolVector: return cdiv(k, 256u);
-    case kKindUpdate: return cdiv(k, T) * cdiv(N, T);
+    case kKindPoly: return tri(cdiv(kp, T));
+    case kKindAolVector: return cdiv(kp, 256u);
+    case kKindUpdate: return cdiv(kp, T) * cdiv(Np, T);
     case kKindApplyScale:
     case kKindCopyOut: return uint32_t((uint64_t(k) * N + kElemBlock - 1) / kElemBlock);
+    case kKindScaleA: return uint32_t((uint64_t(kp) * kp + kElemBlock - 1) / kElemBlock);
   }
   return 0;
 }
@@ -99,21 +104,38 @@ struct WsLayout {
   uint64_t w1, w2, a, b, a32, s, part, fpart, total;
 };
 
-// Byte offsets of the sub-buffers of one matrix's workspace region.
-TM_HD WsLayout ws_layout(uint32_t k, uint32_t N, uint32_t esz) {
+// Byte offsets of the sub-buffers of one matrix's workspace region, for
+// padded dims kp x Np: Y buffers kp x Np (ld Np), A, B kp x kp (ld kp), the
+// fp32 first Gram kp x kp, s (kp floats), row-sum partials
+// [ceil(kp / 64)][kp] and the Frobenius partials.
+TM_HD WsLayout ws_layout(uint32_t kp, uint32_t Np, uint32_t esz) {
   WsLayout L;
-  const uint64_t y = align256(uint64_t(k) * N * esz);
-  const uint64_t g = align256(uint64_t(k) * kpad(k) * esz);
+  const uint64_t y = align256(uint64_t(kp) * Np * esz);
+  const uint64_t g = align256(uint64_t(kp) * kp * esz);
   L.w1 = 0;
   L.w2 = L.w1 + y;
   L.a = L.w2 + y;
   L.b = L.a + g;
   L.a32 = L.b + g;
-  L.s = L.a32 + align256(uint64_t(k) * kpad(k) * 4u);
-  L.part = L.s + align256(uint64_t(k) * 4u);
-  L.fpart = L.part + align256(uint64_t(cdiv(k, kMinTile)) * k * 4u);
+  L.s = L.a32 + align256(uint64_t(kp) * kp * 4u);
+  L.part = L.s + align256(uint64_t(kp) * 4u);
+  L.fpart = L.part + align256(uint64_t(cdiv(kp, kMinTile)) * kp * 4u);
   L.total = L.fpart + align256(uint64_t(kFrobBlocks) * 4u);
   return L;
+}
+
+// Padded dims of the generic (fp32) path: A and B rows padded to 8 for
+// 16-byte row alignment, Y unpadded.
+TM_HD void generic_dims(uint32_t k, uint32_t N, uint32_t* kp, uint32_t* Np) {
+  *kp = kpad(k);
+  *Np = N;
+}
+
+// Padded dims of the bf16 matrix-core path with square tiles of size T:
+// every tile is full and the padding is kept at zero.
+TM_HD void tiled_dims(uint32_t k, uint32_t N, uint32_t T, uint32_t* kp, uint32_t* Np) {
+  *kp = cdiv(k, T) * T;
+  *Np = cdiv(N, T) * T;
 }
 
 }  // namespace tmk

@@ -90,7 +90,7 @@ __device__ inline Loc locate(const Phase& P, int lid) {
 
 template <typename T>
 __device__ inline char* ws_of(const Phase& P, const Entry& E, int mat) {
-  const WsLayout L = ws_layout(E.k, E.N, sizeof(T));
+  const WsLayout L = ws_layout(E.kp, E.Np, sizeof(T));
   return P.ws + E.ws + uint64_t(mat) * L.total;
 }
 
@@ -105,7 +105,7 @@ __device__ inline T* slot_ptr(const Phase& P, const Entry& E, int mat, int slot)
   const bool tall = (E.flags & kTall) != 0u;
   if (!tall && (slot == kSlotFirst || slot == kSlotFinal)) return user_of<T>(E, mat);
   if (tall && slot == kSlotFinal) return user_of<T>(E, mat);
-  const WsLayout L = ws_layout(E.k, E.N, sizeof(T));
+  const WsLayout L = ws_layout(E.kp, E.Np, sizeof(T));
   char* w = ws_of<T>(P, E, mat);
   const bool w1 = tall ? (slot == kSlotFirst || slot == kSlotAlt2) : (slot == kSlotAlt1);
   return reinterpret_cast<T*>(w + (w1 ? L.w1 : L.w2));
@@ -416,12 +416,12 @@ __global__ __launch_bounds__(256) void k_gram(const Phase P) {
                                 vec, Y + int64_t(J) * C::BN * N, N, min(C::BN, k - J * C::BN), vec,
                                 N, nullptr, nullptr, nullptr);
   char* w = ws_of<T>(P, E, L.mat);
-  const WsLayout WL = ws_layout(E.k, E.N, sizeof(T));
+  const WsLayout WL = ws_layout(E.kp, E.Np, sizeof(T));
   auto ident = [](int, int, float x) { return x; };
   if (P.flags & kA32)   // first iteration: keep A0 unrounded until it is rescaled
-    store_sym<float, C>(acc, reinterpret_cast<float*>(w + WL.a32), kpad(E.k), k, I, J, ident, ident);
+    store_sym<float, C>(acc, reinterpret_cast<float*>(w + WL.a32), E.kp, k, I, J, ident, ident);
   else
-    store_sym<T, C>(acc, reinterpret_cast<T*>(w + WL.a), kpad(E.k), k, I, J, ident, ident);
+    store_sym<T, C>(acc, reinterpret_cast<T*>(w + WL.a), E.kp, k, I, J, ident, ident);
 
   if (P.flags & kRowSum) {
     float* part = reinterpret_cast<float*>(w + WL.part);
@@ -454,9 +454,9 @@ __global__ __launch_bounds__(256) void k_gram(const Phase P) {
     __syncthreads();
     for (int r = threadIdx.x; r < C::BM; r += 256) {
       const int i = I * C::BM + r;
-      if (i < k) part[int64_t(J) * k + i] = rs[r] + rs[C::BM + r];
+      if (i < k) part[int64_t(J) * E.kp + i] = rs[r] + rs[C::BM + r];
       const int j = J * C::BN + r;
-      if (I != J && j < k) part[int64_t(I) * k + j] = cs[r] + cs[C::BN + r];
+      if (I != J && j < k) part[int64_t(I) * E.kp + j] = cs[r] + cs[C::BN + r];
     }
   }
 }
@@ -474,10 +474,10 @@ __global__ __launch_bounds__(256) void k_poly(const Phase P) {
   int I, J;
   tri_tile(L.tile, int(cdiv(E.k, C::BM)), I, J);
   char* w = ws_of<T>(P, E, L.mat);
-  const WsLayout WL = ws_layout(E.k, E.N, sizeof(T));
+  const WsLayout WL = ws_layout(E.kp, E.Np, sizeof(T));
   T* B = reinterpret_cast<T*>(w + WL.b);
   const float* s = reinterpret_cast<const float*>(w + WL.s);
-  const int64_t ld = kpad(E.k);
+  const int64_t ld = E.kp;
   const float b = P.b, c = P.c;
   f32x16_t acc[C::FM][C::FN];
   if constexpr (SCALE) {
@@ -524,13 +524,13 @@ __global__ __launch_bounds__(256) void k_update(const Phase P) {
   const int Lb = rem / gsz;
 
   char* w = ws_of<T>(P, E, L.mat);
-  const WsLayout WL = ws_layout(E.k, E.N, sizeof(T));
+  const WsLayout WL = ws_layout(E.kp, E.Np, sizeof(T));
   const T* B = reinterpret_cast<const T*>(w + WL.b);
   const float* s = reinterpret_cast<const float*>(w + WL.s);
   const T* Y = slot_ptr<T>(P, E, L.mat, P.src);
   T* D = slot_ptr<T>(P, E, L.mat, P.dst);
   const bool vec = (N % Elem<T>::VE) == 0 && aligned16(Y);
-  const int64_t ldb = kpad(E.k);
+  const int64_t ldb = E.kp;
   f32x16_t acc[C::FM][C::FN];
   gemm_tile<T, C, true, false>(acc, smem, B + int64_t(I) * C::BM * ldb, ldb,
                                min(C::BM, k - I * C::BM), true, Y + int64_t(Lb) * C::BN, N,
@@ -606,7 +606,7 @@ __global__ __launch_bounds__(256) void k_frob_partial(const Phase P) {
   }
   x = block_sum_256(x, red);
   if (threadIdx.x == 0) {
-    float* fp = reinterpret_cast<float*>(ws_of<T>(P, E, L.mat) + ws_layout(E.k, E.N, sizeof(T)).fpart);
+    float* fp = reinterpret_cast<float*>(ws_of<T>(P, E, L.mat) + ws_layout(E.kp, E.Np, sizeof(T)).fpart);
     fp[L.tile] = x;
   }
 }
@@ -617,22 +617,24 @@ template <typename T>
 __global__ __launch_bounds__(256) void k_aol_vector(const Phase P) {
   const Loc L = locate(P, blockIdx.x);
   const Entry& E = P.e[L.ent];
-  const int k = int(E.k);
+  const int k = int(E.k), kp = int(E.kp);
   const int i = L.tile * 256 + int(threadIdx.x);
-  if (i >= k) return;
+  if (i >= kp) return;
   char* w = ws_of<T>(P, E, L.mat);
-  const WsLayout WL = ws_layout(E.k, E.N, sizeof(T));
+  const WsLayout WL = ws_layout(E.kp, E.Np, sizeof(T));
   float* s = reinterpret_cast<float*>(w + WL.s);
   float r = 0.f;
-  if (P.flags & kFrob) {
-    const float* fp = reinterpret_cast<const float*>(w + WL.fpart);
-    for (int b = 0; b < kFrobBlocks; ++b) r += fp[b];
-  } else {
-    const float* part = reinterpret_cast<const float*>(w + WL.part);
-    const int nb = int(cdiv(E.k, uint32_t(P.aux)));
-    for (int b = 0; b < nb; ++b) r += part[int64_t(b) * k + i];
+  if (i < k) {
+    if (P.flags & kFrob) {
+      const float* fp = reinterpret_cast<const float*>(w + WL.fpart);
+      for (int b = 0; b < kFrobBlocks; ++b) r += fp[b];
+    } else {
+      const float* part = reinterpret_cast<const float*>(w + WL.part);
+      const int nb = int(cdiv(E.kp, uint32_t(P.aux)));
+      for (int b = 0; b < nb; ++b) r += part[int64_t(b) * kp + i];
+    }
   }
-  s[i] = r >= 1.17549435e-38f ? 1.0f / sqrtf(r) : 0.f;
+  s[i] = r >= 1.17549435e-38f ? 1.0f / sqrtf(r) : 0.f;   // padding rows: 0
 }
 
 // X1 = diag(s) X0 in place on the user matrix (rows of the wide view).
@@ -643,7 +645,7 @@ __global__ __launch_bounds__(256) void k_apply_scale(const Phase P) {
   const int64_t total = int64_t(E.k) * E.N;
   T* X = user_of<T>(E, L.mat);
   const float* s = reinterpret_cast<const float*>(ws_of<T>(P, E, L.mat) +
-                                                  ws_layout(E.k, E.N, sizeof(T)).s);
+                                                  ws_layout(E.kp, E.Np, sizeof(T)).s);
   const bool tall = (E.flags & kTall) != 0u;
   const int64_t lo = int64_t(L.tile) * kElemBlock;
   for (int64_t idx = lo + threadIdx.x; idx < min(total, lo + kElemBlock); idx += 256) {
@@ -693,18 +695,24 @@ static hipError_t update_t(int cfg, const Phase& P, hipStream_t st) {
 }
 
 #ifndef TM_ELEM_BYTES
-#define TM_ELEM_BYTES 2
+#define TM_ELEM_BYTES 4
 #endif
 
 #if TM_ELEM_BYTES == 2
-using ElemT = uint16_t;
-hipError_t launch_phase_bf16(int kind, int cfg, const Phase& P, hipStream_t st)
+// bf16: the elementwise phases; the matrix-core phases live in tm_fast.hip.
+hipError_t launch_elementwise_bf16(int kind, const Phase& P, hipStream_t st) {
+  using T = uint16_t;
+  if (P.total <= 0) return hipSuccess;
+  switch (kind) {
+    case kKindFrob: TM_LAUNCH(k_frob_partial<T>);
+    case kKindAolVector: TM_LAUNCH(k_aol_vector<T>);
+    case kKindApplyScale: TM_LAUNCH(k_apply_scale<T>);
+  }
+  return hipErrorInvalidValue;
+}
 #else
-using ElemT = float;
-hipError_t launch_phase_f32(int kind, int cfg, const Phase& P, hipStream_t st)
-#endif
-{
-  using T = ElemT;
+hipError_t launch_phase_f32(int kind, int cfg, const Phase& P, hipStream_t st) {
+  using T = float;
   if (P.total <= 0) return hipSuccess;
   const bool scale = (P.flags & kScale) != 0u;
   switch (kind) {
@@ -719,5 +727,6 @@ hipError_t launch_phase_f32(int kind, int cfg, const Phase& P, hipStream_t st)
   }
   return hipErrorInvalidValue;
 }
+#endif
 
 }  // namespace tmk

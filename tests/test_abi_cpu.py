@@ -100,18 +100,24 @@ def test_grouped_validation(fn):
 
 
 def test_workspace_bytes():
-    # ping-pong Y twice, A and B (k x roundup8(k)), s, row-sum partials, Frobenius partials
+    # per matrix: two Y buffers (kp x Np), A and B (kp x kp), the fp32 first Gram,
+    # s, the row-sum partials [ceil(kp/64)][kp] and 32 Frobenius partials
     def a256(v):
         return (v + 255) // 256 * 256
 
-    def expect(m, n, e):
-        k, N = min(m, n), max(m, n)
-        kp = (k + 7) // 8 * 8
-        return (2 * a256(k * N * e) + 2 * a256(k * kp * e) + a256(4 * k * kp) + a256(4 * k)
-                + a256(4 * k * ((k + 63) // 64)) + a256(4 * 32))
+    def layout(kp, Np, e):
+        return (2 * a256(kp * Np * e) + 2 * a256(kp * kp * e) + a256(4 * kp * kp) + a256(4 * kp)
+                + a256(4 * kp * ((kp + 63) // 64)) + a256(4 * 32))
 
     shapes = [(768, 3072), (3072, 768), (17, 33), (1, 1)]
-    for e in (2, 4):
-        assert tm.workspace_bytes(shapes, e) == sum(expect(m, n, e) for m, n in shapes)
+    # fp32: A and B rows padded to 8, Y unpadded
+    f32 = sum(layout((min(m, n) + 7) // 8 * 8, max(m, n), 4) for m, n in shapes)
+    assert tm.workspace_bytes(shapes, 4) == f32
+    # bf16: every dim padded to the call's square tile T (one of 256, 128, 64)
+    bf = tm.workspace_bytes(shapes, 2)
+    cands = [sum(layout(-(-min(m, n) // T) * T, -(-max(m, n) // T) * T, 2) for m, n in shapes)
+             for T in (256, 128, 64)]
+    assert bf in cands
+    assert tm.workspace_bytes([(4096, 14336)], 2) == layout(4096, 14336, 2)
     assert tm.workspace_bytes([(0, 4)], 2) == 0
     assert tm.workspace_bytes([(4, 4)], 3) == 0
