@@ -11,10 +11,9 @@
 //                 the fp32 accumulators are stored instead (A0 is rescaled
 //                 before rounding) and the epilogue emits the AOL row sums
 //                 sum_j |A0_ij| (eq. (aol))
-//   k_scale_a     A1 = diag(s) A0 diag(s), rounded once to bf16
-//   k_poly_fast   B~ = b A + c A A + a I, upper tiles, mirrored store; at
-//                 iteration 1 the stored matrix is B~ diag(s), which applies
-//                 X1 = diag(s) X0 inside the next product
+//   k_apply_s     A1 = diag(s) A0 diag(s) and X1 = diag(s) X0, each rounded
+//                 once to bf16
+//   k_poly_fast   B~ = b A + c A A + a I, upper tiles, mirrored store
 //   k_update_fast Y' = B~ Y = a Y + B Y: the axpy of the update rides on B~'s
 //                 diagonal, so the update is a single product with no second
 //                 read of Y
@@ -41,8 +40,11 @@ typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x16_t __attribute__((ext_vector_type(16)));
 typedef short s16x4_t __attribute__((ext_vector_type(4)));
 
+#ifndef TM_FAST_STAGES
+#define TM_FAST_STAGES 4
+#endif
 constexpr int BK = 32;        // K elements per stage (64 bytes of a K-contiguous row)
-constexpr int STAGES = 4;
+constexpr int STAGES = TM_FAST_STAGES;
 
 template <int T>
 struct Tile {
@@ -51,6 +53,7 @@ struct Tile {
   static constexpr int A_BYTES = T * BK * 2;    // one operand stage
   static constexpr int STAGE = 2 * A_BYTES;
   static constexpr int LDS = STAGES * STAGE;
+  static_assert(LDS <= 160 * 1024, "gfx950 LDS is 160 KB per workgroup");
   static constexpr int PER_STAGE = T / 32;      // DMA instructions per wave per stage
 };
 
@@ -79,15 +82,37 @@ __device__ inline void dma16(const void* base, uint32_t voff, uint32_t lds) {
 }
 
 // Wait until at most `pending` DMA instructions of this wave are in flight and
-// all of its LDS reads are done, then join the workgroup barrier.
+// all of its LDS reads are done, then join the workgroup barrier.  The LDS
+// wait goes through the builtin so that the compiler knows the reads are
+// complete; the DMA wait and the barrier are assembly, since the compiler does
+// not see the DMA loads.
+template <int PENDING>
+__device__ inline void ring_sync_dma() {
+  if constexpr (PENDING == 0) asm volatile("s_waitcnt vmcnt(0)\n\ts_barrier" ::: "memory");
+  else if constexpr (PENDING == 2) asm volatile("s_waitcnt vmcnt(2)\n\ts_barrier" ::: "memory");
+  else if constexpr (PENDING == 4) asm volatile("s_waitcnt vmcnt(4)\n\ts_barrier" ::: "memory");
+  else if constexpr (PENDING == 6) asm volatile("s_waitcnt vmcnt(6)\n\ts_barrier" ::: "memory");
+  else if constexpr (PENDING == 8) asm volatile("s_waitcnt vmcnt(8)\n\ts_barrier" ::: "memory");
+  else if constexpr (PENDING == 12) asm volatile("s_waitcnt vmcnt(12)\n\ts_barrier" ::: "memory");
+  else if constexpr (PENDING == 16) asm volatile("s_waitcnt vmcnt(16)\n\ts_barrier" ::: "memory");
+  else if constexpr (PENDING == 24) asm volatile("s_waitcnt vmcnt(24)\n\ts_barrier" ::: "memory");
+  else static_assert(PENDING == 0, "unsupported in-flight count");
+}
+
 template <int PENDING>
 __device__ inline void ring_sync() {
-  if constexpr (PENDING == 0) asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory");
-  else if constexpr (PENDING == 2) asm volatile("s_waitcnt vmcnt(2) lgkmcnt(0)\n\ts_barrier" ::: "memory");
-  else if constexpr (PENDING == 4) asm volatile("s_waitcnt vmcnt(4) lgkmcnt(0)\n\ts_barrier" ::: "memory");
-  else if constexpr (PENDING == 8) asm volatile("s_waitcnt vmcnt(8) lgkmcnt(0)\n\ts_barrier" ::: "memory");
-  else if constexpr (PENDING == 16) asm volatile("s_waitcnt vmcnt(16) lgkmcnt(0)\n\ts_barrier" ::: "memory");
-  else static_assert(PENDING == 0, "unsupported in-flight count");
+  __builtin_amdgcn_s_waitcnt(0xC07F);   // lgkmcnt(0), vmcnt/expcnt untouched
+  ring_sync_dma<PENDING>();
+}
+
+// Wait for all but `stages` of this wave's stages in flight, then barrier.
+template <int PS>
+__device__ inline void ring_wait(int stages) {
+  __builtin_amdgcn_s_waitcnt(0xC07F);   // lgkmcnt(0), vmcnt/expcnt untouched
+  if (stages >= 3) ring_sync_dma<3 * PS>();
+  else if (stages == 2) ring_sync_dma<2 * PS>();
+  else if (stages == 1) ring_sync_dma<PS>();
+  else ring_sync_dma<0>();
 }
 
 // ---------------------------------------------------------------- DMA issue
@@ -131,60 +156,83 @@ __device__ inline void issue_rm(const uint16_t* src, int64_t ld, int k0, uint32_
 }
 
 // ---------------------------------------------------------------- compute
+template <int T>
+struct Frags {
+  uint4 a[Tile<T>::F], b[Tile<T>::F];
+};
+
+// MFMA operands of K slice kk (16 wide) of one stage.
 template <int T, bool RM>
-__device__ inline void compute_stage(f32x16_t (&acc)[Tile<T>::F][Tile<T>::F], const char* sa,
-                                     const char* sb, int wm, int wn) {
+__device__ inline void load_frags(Frags<T>& fr, const char* sa, const char* sb, int kk, int wm,
+                                  int wn) {
   constexpr int F = Tile<T>::F, TW = Tile<T>::TW;
   const int lane = threadIdx.x & 63;
   const int lr = lane & 31, lh = lane >> 5;
+  const int c = 2 * kk + lh;
 #pragma unroll
-  for (int kk = 0; kk < BK / 16; ++kk) {
-    uint4 a[F], b[F];
-    const int c = 2 * kk + lh;
+  for (int f = 0; f < F; ++f) {
+    const int r = wm * TW + f * 32 + lr;
+    fr.a[f] = *reinterpret_cast<const uint4*>(sa + r * 64 + 16 * (c ^ ((r >> 2) & 3)));
+  }
+  if constexpr (!RM) {
 #pragma unroll
     for (int f = 0; f < F; ++f) {
-      const int r = wm * TW + f * 32 + lr;
-      a[f] = *reinterpret_cast<const uint4*>(sa + r * 64 + 16 * (c ^ ((r >> 2) & 3)));
+      const int r = wn * TW + f * 32 + lr;
+      fr.b[f] = *reinterpret_cast<const uint4*>(sb + r * 64 + 16 * (c ^ ((r >> 2) & 3)));
     }
-    if constexpr (!RM) {
+  } else {
+    // Lane q of 16-lane group g addresses row kb + q/4, columns n + 4(q%4);
+    // the transposed read returns rows kb..kb+3 of column n + q.
+    const int g = lane >> 4, q = lane & 15;
+    const int kb = 16 * kk + 8 * (g >> 1) + (q >> 2);
 #pragma unroll
-      for (int f = 0; f < F; ++f) {
-        const int r = wn * TW + f * 32 + lr;
-        b[f] = *reinterpret_cast<const uint4*>(sb + r * 64 + 16 * (c ^ ((r >> 2) & 3)));
+    for (int f = 0; f < F; ++f) {
+      const int chunk = (wn * TW + f * 32) / 16 + (g & 1);
+      s16x4_t v[2];
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        const int row = kb + 4 * h;
+        const char* p = sb + row * (2 * T) + 32 * (chunk ^ swz_y<T>(row)) + 8 * (q & 3);
+        v[h] = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+            (__attribute__((address_space(3))) s16x4_t*)(lds_addr(p)));
       }
-    } else {
-      // Lane q of 16-lane group g addresses row kb + q/4, columns n + 4(q%4);
-      // the transposed read returns rows kb..kb+3 of column n + q.
-      const int g = lane >> 4, q = lane & 15;
-      const int kb = 16 * kk + 8 * (g >> 1) + (q >> 2);
-#pragma unroll
-      for (int f = 0; f < F; ++f) {
-        const int chunk = (wn * TW + f * 32) / 16 + (g & 1);
-        s16x4_t v[2];
-#pragma unroll
-        for (int h = 0; h < 2; ++h) {
-          const int row = kb + 4 * h;
-          const char* p = sb + row * (2 * T) + 32 * (chunk ^ swz_y<T>(row)) + 8 * (q & 3);
-          v[h] = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-              (__attribute__((address_space(3))) s16x4_t*)(lds_addr(p)));
-        }
-        b[f] = __builtin_bit_cast(uint4, v);
-      }
+      fr.b[f] = __builtin_bit_cast(uint4, v);
     }
-#pragma unroll
-    for (int fm = 0; fm < F; ++fm)
-#pragma unroll
-      for (int fn = 0; fn < F; ++fn)
-        acc[fm][fn] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-            __builtin_bit_cast(bf16x8_t, a[fm]), __builtin_bit_cast(bf16x8_t, b[fn]), acc[fm][fn],
-            0, 0, 0);
   }
+}
+
+// SWAP = false: acc[fm][fn] holds C block (fm, fn) in the MFMA layout (lane
+// L, element v: row 8(v/4) + 4(L/32) + v%4, column L%32).  SWAP = true feeds
+// the operands the other way round, so acc[fm][fn] holds the transposed block:
+// each lane then owns 4 consecutive columns of one C row.
+template <int T, bool SWAP>
+__device__ inline void mma(f32x16_t (&acc)[Tile<T>::F][Tile<T>::F], const Frags<T>& fr) {
+  constexpr int F = Tile<T>::F;
+#pragma unroll
+  for (int fm = 0; fm < F; ++fm)
+#pragma unroll
+    for (int fn = 0; fn < F; ++fn) {
+      if constexpr (SWAP)
+        acc[fm][fn] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+            __builtin_bit_cast(bf16x8_t, fr.b[fn]), __builtin_bit_cast(bf16x8_t, fr.a[fm]),
+            acc[fm][fn], 0, 0, 0);
+      else
+        acc[fm][fn] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+            __builtin_bit_cast(bf16x8_t, fr.a[fm]), __builtin_bit_cast(bf16x8_t, fr.b[fn]),
+            acc[fm][fn], 0, 0, 0);
+    }
 }
 
 // acc = A (T x K, K-contiguous rows of a) * B^T where B's rows are the
 // K-contiguous rows of b (RM = false) or B = the K x T row-major block of b
 // (RM = true).  K is a multiple of BK; every tile is full.
-template <int T, bool RM>
+//
+// Schedule per stage kt (two K slices of 16): the operands of slice 0 were
+// read before the stage began; slice 1 is read while slice 0's MFMAs run;
+// then the ring is synchronised for stage kt+1 (its DMA done in every wave,
+// and every wave done reading stage kt), the DMA of stage kt+4 reuses stage
+// kt's buffer, and slice 0 of stage kt+1 is read while slice 1's MFMAs run.
+template <int T, bool RM, bool SWAP = false>
 __device__ inline void mainloop(f32x16_t (&acc)[Tile<T>::F][Tile<T>::F], char* smem,
                                 const uint16_t* a, int64_t lda, const uint16_t* b, int64_t ldb,
                                 int K) {
@@ -206,19 +254,31 @@ __device__ inline void mainloop(f32x16_t (&acc)[Tile<T>::F][Tile<T>::F], char* s
     if constexpr (RM) issue_rm<T>(b, ldb, kt * BK, st + Tile<T>::A_BYTES);
     else issue_kc<T>(b, ldb, kt * BK, st + Tile<T>::A_BYTES);
   };
+  auto stage_ptr = [&](int kt) { return smem + (kt % STAGES) * Tile<T>::STAGE; };
 #pragma unroll
-  for (int s = 0; s < STAGES - 1; ++s)
+  for (int s = 0; s < STAGES; ++s)
     if (s < nk) issue(s);
+  ring_wait<PS>(min(nk - 1, STAGES - 1));
 
-  for (int kt = 0; kt < nk; ++kt) {
-    // stages kt+1 .. kt+2 may stay in flight
-    const int ahead = min(nk - 1, kt + STAGES - 2) - kt;
-    if (ahead >= 2) ring_sync<2 * PS>();
-    else if (ahead == 1) ring_sync<PS>();
-    else ring_sync<0>();
-    if (kt + STAGES - 1 < nk) issue(kt + STAGES - 1);
-    const char* st = smem + (kt % STAGES) * Tile<T>::STAGE;
-    compute_stage<T, RM>(acc, st, st + Tile<T>::A_BYTES, wm, wn);
+  Frags<T> f0, f1;
+  load_frags<T, RM>(f0, stage_ptr(0), stage_ptr(0) + Tile<T>::A_BYTES, 0, wm, wn);
+  for (int kt = 0; kt + 1 < nk; ++kt) {
+    const char* st = stage_ptr(kt);
+    load_frags<T, RM>(f1, st, st + Tile<T>::A_BYTES, 1, wm, wn);
+    mma<T, SWAP>(acc, f0);
+    __builtin_amdgcn_sched_barrier(0);
+    ring_wait<PS>(min(nk - 1, kt + STAGES - 1) - (kt + 1));
+    if (kt + STAGES < nk) issue(kt + STAGES);
+    const char* nx = stage_ptr(kt + 1);
+    load_frags<T, RM>(f0, nx, nx + Tile<T>::A_BYTES, 0, wm, wn);
+    __builtin_amdgcn_sched_barrier(0);
+    mma<T, SWAP>(acc, f1);
+  }
+  {
+    const char* st = stage_ptr(nk - 1);
+    load_frags<T, RM>(f1, st, st + Tile<T>::A_BYTES, 1, wm, wn);
+    mma<T, SWAP>(acc, f0);
+    mma<T, SWAP>(acc, f1);
   }
   ring_sync<0>();   // the ring is free for the epilogue
 }
@@ -280,12 +340,150 @@ __device__ inline int acc_col(int wn, int fn) {
   return wn * Tile<T>::TW + fn * 32 + (threadIdx.x & 31);
 }
 
-// Store tile (I, J) of a symmetric kp x kp matrix (ld kp) and, off the
-// diagonal, its transpose at (J, I).  f gives the value stored at (i, j), g the
-// one stored at the mirrored (j, i).
-template <int T, typename OUT, class Fv, class Gv>
-__device__ inline void store_sym(const f32x16_t (&acc)[Tile<T>::F][Tile<T>::F], OUT* D, int64_t ld,
-                                 int I, int J, Fv f, Gv g) {
+// ---------------------------------------------------------------- epilogues
+// Output tiles are staged through LDS (the ring is free after the main loop)
+// as T x T bf16 with rows padded to T + 8 elements, so that global stores are
+// full 16-byte vectors along contiguous rows.
+template <int T>
+struct Stage {
+  static constexpr int RS = (T + 8) * 2;            // padded row stride in bytes
+  static constexpr int BYTES = T * RS;
+  static constexpr int CPR = T / 8;                 // 16-byte chunks per row
+  static constexpr int PER_THREAD = T * CPR / 256;  // chunks per thread
+};
+
+template <int T>
+constexpr int smem_bytes() {
+  return Tile<T>::LDS > Stage<T>::BYTES ? Tile<T>::LDS : Stage<T>::BYTES;
+}
+
+// LDS row r of the stage -> dst row row0 + r, columns col0.. (whole tile).
+template <int T>
+__device__ inline void store_rows(const char* st, uint16_t* dst, int64_t ld, int64_t row0,
+                                  int64_t col0) {
+#pragma unroll 4
+  for (int it = 0; it < Stage<T>::PER_THREAD; ++it) {
+    const int q = it * 256 + int(threadIdx.x);
+    const int r = q / Stage<T>::CPR, c8 = q % Stage<T>::CPR;
+    const uint4 v = *reinterpret_cast<const uint4*>(st + r * Stage<T>::RS + c8 * 16);
+    *reinterpret_cast<uint4*>(dst + (row0 + r) * ld + col0 + c8 * 8) = v;
+  }
+}
+
+// Transposed: stage element (r, c) -> dst row row0 + c, column col0 + r.
+template <int T>
+__device__ inline void store_cols(const char* st, uint16_t* dst, int64_t ld, int64_t row0,
+                                  int64_t col0) {
+#pragma unroll 2
+  for (int it = 0; it < Stage<T>::PER_THREAD; ++it) {
+    const int q = it * 256 + int(threadIdx.x);
+    const int c = q / Stage<T>::CPR, r8 = q % Stage<T>::CPR;
+    uint16_t v[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e)
+      v[e] = *reinterpret_cast<const uint16_t*>(st + (r8 * 8 + e) * Stage<T>::RS + c * 2);
+    *reinterpret_cast<uint4*>(dst + (row0 + c) * ld + col0 + r8 * 8) =
+        *reinterpret_cast<const uint4*>(v);
+  }
+}
+
+// Caller's wide matrix (rows < k, columns < N, ld = N).
+template <int T>
+__device__ inline void store_rows_user(const char* st, uint16_t* dst, int k, int N, int row0,
+                                       int col0) {
+  const bool vec = (N % 8) == 0 && (reinterpret_cast<uintptr_t>(dst) & 15u) == 0u;
+#pragma unroll 2
+  for (int it = 0; it < Stage<T>::PER_THREAD; ++it) {
+    const int q = it * 256 + int(threadIdx.x);
+    const int r = q / Stage<T>::CPR, c8 = q % Stage<T>::CPR;
+    const int i = row0 + r, l = col0 + c8 * 8;
+    if (i >= k || l >= N) continue;
+    const uint4 v = *reinterpret_cast<const uint4*>(st + r * Stage<T>::RS + c8 * 16);
+    uint16_t* p = dst + int64_t(i) * N + l;
+    if (vec && l + 8 <= N) {
+      *reinterpret_cast<uint4*>(p) = v;
+    } else {
+      const uint16_t* e = reinterpret_cast<const uint16_t*>(&v);
+      for (int u = 0; u < 8 && l + u < N; ++u) p[u] = e[u];
+    }
+  }
+}
+
+// Caller's tall matrix: stage element (i, l) of the wide view -> dst[l * k + i].
+template <int T>
+__device__ inline void store_cols_user(const char* st, uint16_t* dst, int k, int N, int row0,
+                                       int col0) {
+  const bool vec = (k % 8) == 0 && (reinterpret_cast<uintptr_t>(dst) & 15u) == 0u;
+#pragma unroll 2
+  for (int it = 0; it < Stage<T>::PER_THREAD; ++it) {
+    const int q = it * 256 + int(threadIdx.x);
+    const int c = q / Stage<T>::CPR, r8 = q % Stage<T>::CPR;
+    const int l = col0 + c, i = row0 + r8 * 8;
+    if (l >= N || i >= k) continue;
+    uint16_t v[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e)
+      v[e] = *reinterpret_cast<const uint16_t*>(st + (r8 * 8 + e) * Stage<T>::RS + c * 2);
+    uint16_t* p = dst + int64_t(l) * k + i;
+    if (vec && i + 8 <= k) {
+      *reinterpret_cast<uint4*>(p) = *reinterpret_cast<const uint4*>(v);
+    } else {
+      for (int u = 0; u < 8 && i + u < k; ++u) p[u] = v[u];
+    }
+  }
+}
+
+// Global rows row0.. (T x T bf16 block at col0, ld) -> stage rows.
+template <int T>
+__device__ inline void load_rows(char* st, const uint16_t* src, int64_t ld, int64_t row0,
+                                 int64_t col0) {
+#pragma unroll 4
+  for (int it = 0; it < Stage<T>::PER_THREAD; ++it) {
+    const int q = it * 256 + int(threadIdx.x);
+    const int r = q / Stage<T>::CPR, c8 = q % Stage<T>::CPR;
+    *reinterpret_cast<uint4*>(st + r * Stage<T>::RS + c8 * 16) =
+        *reinterpret_cast<const uint4*>(src + (row0 + r) * ld + col0 + c8 * 8);
+  }
+}
+
+// Symmetric-product epilogue (Gram, polynomial): value f(i_local, j_local, x,
+// staged) of C element (i, j) is written transposed into the stage as
+// (j, i); the stage then holds tile (J, I), stored as rows of block J and,
+// off the diagonal, transposed as tile (I, J).  `staged` is the stage's
+// previous bf16 at that position (the polynomial preloads A's tile (J, I)).
+template <int T, class Fv>
+__device__ inline void epilogue_sym(const f32x16_t (&acc)[Tile<T>::F][Tile<T>::F], char* st,
+                                    uint16_t* D, int64_t ld, int I, int J, Fv f) {
+  constexpr int F = Tile<T>::F;
+  const int wave = threadIdx.x >> 6;
+  const int wm = wave >> 1, wn = wave & 1;
+#pragma unroll
+  for (int fm = 0; fm < F; ++fm)
+#pragma unroll
+    for (int fn = 0; fn < F; ++fn) {
+      const int c = acc_col<T>(wn, fn);
+#pragma unroll
+      for (int v4 = 0; v4 < 4; ++v4) {
+        const int r0 = acc_row<T>(wm, fm, 4 * v4);
+        char* p = st + c * Stage<T>::RS + r0 * 2;
+        const uint2 old = *reinterpret_cast<const uint2*>(p);
+        const uint16_t* o = reinterpret_cast<const uint16_t*>(&old);
+        uint16_t out[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) out[u] = f2bf(f(r0 + u, c, acc[fm][fn][4 * v4 + u], o[u]));
+        *reinterpret_cast<uint2*>(p) = *reinterpret_cast<const uint2*>(out);
+      }
+    }
+  __syncthreads();
+  store_rows<T>(st, D, ld, int64_t(J) * T, int64_t(I) * T);
+  if (I != J) store_cols<T>(st, D, ld, int64_t(I) * T, int64_t(J) * T);
+}
+
+// fp32 store of a symmetric tile and its mirror straight from the registers
+// (first Gram only).
+template <int T>
+__device__ inline void store_sym_f32(const f32x16_t (&acc)[Tile<T>::F][Tile<T>::F], float* D,
+                                     int64_t ld, int I, int J) {
   constexpr int F = Tile<T>::F;
   const int wave = threadIdx.x >> 6;
   const int wm = wave >> 1, wn = wave & 1;
@@ -297,24 +495,13 @@ __device__ inline void store_sym(const f32x16_t (&acc)[Tile<T>::F][Tile<T>::F], 
 #pragma unroll
       for (int v4 = 0; v4 < 4; ++v4) {
         const int ib = I * T + acc_row<T>(wm, fm, 4 * v4);
-        OUT o[4], m[4];
+        float m[4];
 #pragma unroll
         for (int u = 0; u < 4; ++u) {
-          const float x = acc[fm][fn][4 * v4 + u];
-          if constexpr (sizeof(OUT) == 2) {
-            o[u] = f2bf(f(ib + u, j, x));
-            m[u] = f2bf(g(ib + u, j, x));
-          } else {
-            o[u] = f(ib + u, j, x);
-            m[u] = g(ib + u, j, x);
-          }
+          m[u] = acc[fm][fn][4 * v4 + u];
+          D[int64_t(ib + u) * ld + j] = m[u];
         }
-#pragma unroll
-        for (int u = 0; u < 4; ++u) D[int64_t(ib + u) * ld + j] = o[u];
-        if (I != J) {
-          if constexpr (sizeof(OUT) == 2) *reinterpret_cast<uint2*>(D + int64_t(j) * ld + ib) = *reinterpret_cast<uint2*>(m);
-          else *reinterpret_cast<uint4*>(D + int64_t(j) * ld + ib) = *reinterpret_cast<uint4*>(m);
-        }
+        if (I != J) *reinterpret_cast<float4*>(D + int64_t(j) * ld + ib) = *reinterpret_cast<const float4*>(m);
       }
     }
 }
@@ -322,7 +509,7 @@ __device__ inline void store_sym(const f32x16_t (&acc)[Tile<T>::F][Tile<T>::F], 
 // ---------------------------------------------------------------- kernels
 template <int T>
 __global__ __launch_bounds__(256) void k_gram_fast(const Phase P) {
-  __shared__ __attribute__((aligned(1024))) char smem[Tile<T>::LDS];
+  __shared__ __attribute__((aligned(1024))) char smem[smem_bytes<T>()];
   constexpr int F = Tile<T>::F;
   const Loc L = locate(P, xcd_remap(blockIdx.x, P.total));
   const Entry& E = P.e[L.ent];
@@ -335,14 +522,16 @@ __global__ __launch_bounds__(256) void k_gram_fast(const Phase P) {
 
   char* w = ws_of(P, E, L.mat);
   const WsLayout WL = ws_layout(E.kp, E.Np, 2);
-  auto ident = [](int, int, float x) { return x; };
-  if (P.flags & kA32)
-    store_sym<T, float>(acc, reinterpret_cast<float*>(w + WL.a32), kp, I, J, ident, ident);
-  else
-    store_sym<T, uint16_t>(acc, reinterpret_cast<uint16_t*>(w + WL.a), kp, I, J, ident, ident);
+  if (P.flags & kA32) {
+    store_sym_f32<T>(acc, reinterpret_cast<float*>(w + WL.a32), kp, I, J);
+  } else {
+    auto f = [](int, int, float x, uint16_t) { return x; };
+    epilogue_sym<T>(acc, smem, reinterpret_cast<uint16_t*>(w + WL.a), kp, I, J, f);
+  }
 
   if (P.flags & kRowSum) {
     // part[Jb][i] = sum over column block Jb of |A0_ij|, from the fp32 accumulators
+    __syncthreads();
     float* part = reinterpret_cast<float*>(w + WL.part);
     float* rs = reinterpret_cast<float*>(smem);       // [2][T] row sums per wn
     float* cs = rs + 2 * T;                           // [2][T] column sums per wm
@@ -377,12 +566,11 @@ __global__ __launch_bounds__(256) void k_gram_fast(const Phase P) {
   }
 }
 
-// B~ = b A + c A A + a I (upper tiles, mirrored).  SCALE: A1 = diag(s) A0 diag(s)
-// comes in rounded in A (k_scale_a) and unrounded in a32; the stored matrix
-// is B~1 diag(s).
-template <int T, bool SCALE>
+// B~ = b A + c A A + a I (upper tiles, mirrored).  The stage is preloaded with
+// A's tile (J, I), whose element (j, i) equals A_ij.
+template <int T>
 __global__ __launch_bounds__(256) void k_poly_fast(const Phase P) {
-  __shared__ __attribute__((aligned(1024))) char smem[Tile<T>::LDS];
+  __shared__ __attribute__((aligned(1024))) char smem[smem_bytes<T>()];
   constexpr int F = Tile<T>::F;
   const Loc L = locate(P, xcd_remap(blockIdx.x, P.total));
   const Entry& E = P.e[L.ent];
@@ -395,30 +583,23 @@ __global__ __launch_bounds__(256) void k_poly_fast(const Phase P) {
   uint16_t* B = reinterpret_cast<uint16_t*>(w + WL.b);
   f32x16_t acc[F][F];
   mainloop<T, false>(acc, smem, A + int64_t(I) * T * kp, kp, A + int64_t(J) * T * kp, kp, kp);
+  load_rows<T>(smem, A, kp, int64_t(J) * T, int64_t(I) * T);
+  __syncthreads();
   const float a = P.a, b = P.b, c = P.c;
-  if constexpr (SCALE) {
-    const float* A0 = reinterpret_cast<const float*>(w + WL.a32);
-    const float* s = reinterpret_cast<const float*>(w + WL.s);
-    auto val = [=](int i, int j, float x) {
-      const float a1 = A0[int64_t(i) * kp + j] * (s[i] * s[j]);
-      return b * a1 + c * x + (i == j ? a : 0.f);
-    };
-    auto f = [=](int i, int j, float x) { return val(i, j, x) * s[j]; };
-    auto g = [=](int i, int j, float x) { return val(i, j, x) * s[i]; };
-    store_sym<T, uint16_t>(acc, B, kp, I, J, f, g);
-  } else {
-    auto f = [=](int i, int j, float x) {
-      return b * bf2f(A[int64_t(i) * kp + j]) + c * x + (i == j ? a : 0.f);
-    };
-    store_sym<T, uint16_t>(acc, B, kp, I, J, f, f);
-  }
+  const bool diag = I == J;
+  auto f = [=](int i, int j, float x, uint16_t aij) {
+    return b * bf2f(aij) + c * x + ((diag && i == j) ? a : 0.f);
+  };
+  epilogue_sym<T>(acc, smem, B, kp, I, J, f);
 }
 
-// Y' = B~ Y.  dst = kSlotFinal writes the caller's matrix (tall: transposed),
-// otherwise the workspace slot (whole padded tile).
+// Y' = B~ Y.  The operands are fed transposed so that each lane holds 4
+// consecutive columns of an output row; the tile goes out through the stage.
+// dst = kSlotFinal writes the caller's matrix (tall: transposed), otherwise
+// the workspace slot.
 template <int T>
 __global__ __launch_bounds__(256) void k_update_fast(const Phase P) {
-  __shared__ __attribute__((aligned(1024))) char smem[Tile<T>::LDS];
+  __shared__ __attribute__((aligned(1024))) char smem[smem_bytes<T>()];
   constexpr int F = Tile<T>::F;
   const Loc L = locate(P, xcd_remap(blockIdx.x, P.total));
   const Entry& E = P.e[L.ent];
@@ -438,48 +619,33 @@ __global__ __launch_bounds__(256) void k_update_fast(const Phase P) {
   const uint16_t* B = reinterpret_cast<const uint16_t*>(w + WL.b);
   const uint16_t* Y = wbuf(P, E, L.mat, P.src);
   f32x16_t acc[F][F];
-  mainloop<T, true>(acc, smem, B + int64_t(I) * T * kp, kp, Y + int64_t(Lb) * T, Np, kp);
+  mainloop<T, true, true>(acc, smem, B + int64_t(I) * T * kp, kp, Y + int64_t(Lb) * T, Np, kp);
 
-  const int wave = threadIdx.x >> 6;
+  // acc[fm][fn] element v: output row i = wm*TW + fm*32 + lane%32, columns
+  // l0..l0+3 with l0 = wn*TW + fn*32 + 8(v/4) + 4(lane/32)
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int wm = wave >> 1, wn = wave & 1;
-  if (P.dst != kSlotFinal) {
-    uint16_t* D = wbuf(P, E, L.mat, P.dst);
 #pragma unroll
-    for (int fm = 0; fm < F; ++fm)
+  for (int fm = 0; fm < F; ++fm)
 #pragma unroll
-      for (int fn = 0; fn < F; ++fn) {
-        const int l = Lb * T + acc_col<T>(wn, fn);
+    for (int fn = 0; fn < F; ++fn) {
+      const int i = wm * Tile<T>::TW + fm * 32 + (lane & 31);
 #pragma unroll
-        for (int v = 0; v < 16; ++v)
-          D[int64_t(I * T + acc_row<T>(wm, fm, v)) * Np + l] = f2bf(acc[fm][fn][v]);
+      for (int v4 = 0; v4 < 4; ++v4) {
+        const int l0 = wn * Tile<T>::TW + fn * 32 + 8 * v4 + 4 * (lane >> 5);
+        uint16_t out[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) out[u] = f2bf(acc[fm][fn][4 * v4 + u]);
+        *reinterpret_cast<uint2*>(smem + i * Stage<T>::RS + l0 * 2) = *reinterpret_cast<const uint2*>(out);
       }
-  } else if ((E.flags & kTall) == 0u) {
-    uint16_t* D = user_of(E, L.mat);
-#pragma unroll
-    for (int fm = 0; fm < F; ++fm)
-#pragma unroll
-      for (int fn = 0; fn < F; ++fn) {
-        const int l = Lb * T + acc_col<T>(wn, fn);
-#pragma unroll
-        for (int v = 0; v < 16; ++v) {
-          const int i = I * T + acc_row<T>(wm, fm, v);
-          if (i < k && l < N) D[int64_t(i) * N + l] = f2bf(acc[fm][fn][v]);
-        }
-      }
-  } else {
-    uint16_t* D = user_of(E, L.mat);   // N x k: element (i, l) of the wide view at l * k + i
-#pragma unroll
-    for (int fm = 0; fm < F; ++fm)
-#pragma unroll
-      for (int fn = 0; fn < F; ++fn) {
-        const int l = Lb * T + acc_col<T>(wn, fn);
-#pragma unroll
-        for (int v = 0; v < 16; ++v) {
-          const int i = I * T + acc_row<T>(wm, fm, v);
-          if (i < k && l < N) D[int64_t(l) * k + i] = f2bf(acc[fm][fn][v]);
-        }
-      }
-  }
+    }
+  __syncthreads();
+  if (P.dst != kSlotFinal)
+    store_rows<T>(smem, wbuf(P, E, L.mat, P.dst), Np, int64_t(I) * T, int64_t(Lb) * T);
+  else if ((E.flags & kTall) == 0u)
+    store_rows_user<T>(smem, user_of(E, L.mat), k, N, I * T, Lb * T);
+  else
+    store_cols_user<T>(smem, user_of(E, L.mat), k, N, I * T, Lb * T);
 }
 
 // W1 = X (wide) or X^T (tall) in the padded layout, zeros outside the matrix.
@@ -512,24 +678,39 @@ __global__ __launch_bounds__(256) void k_load_in(const Phase P) {
   }
 }
 
-// A = bf16(s_i A0_ij s_j) over the padded kp x kp square; 8 elements per thread.
-__global__ __launch_bounds__(256) void k_scale_a(const Phase P) {
+// First iteration after AOL / Frobenius scaling: A1 = bf16(s_i A0_ij s_j)
+// over the padded kp x kp square and X1 = bf16(s_i X0_il) in place on W1;
+// 8 elements per thread, the A blocks first.
+__global__ __launch_bounds__(256) void k_apply_s(const Phase P) {
   const Loc L = locate(P, blockIdx.x);
   const Entry& E = P.e[L.ent];
-  const int64_t kp = E.kp;
+  const int64_t kp = E.kp, Np = E.Np;
   char* w = ws_of(P, E, L.mat);
   const WsLayout WL = ws_layout(E.kp, E.Np, 2);
-  const float* A0 = reinterpret_cast<const float*>(w + WL.a32);
   const float* s = reinterpret_cast<const float*>(w + WL.s);
-  uint16_t* A = reinterpret_cast<uint16_t*>(w + WL.a);
-  const int64_t idx = int64_t(L.tile) * kElemBlock + int64_t(threadIdx.x) * 8;
-  if (idx >= kp * kp) return;
-  const int64_t i = idx / kp, j = idx - i * kp;   // kp % 8 == 0: the 8 stay in row i
-  const float si = s[i];
-  uint16_t o[8];
+  const int nA = int((kp * kp + kElemBlock - 1) / kElemBlock);
+  if (L.tile < nA) {
+    const int64_t idx = int64_t(L.tile) * kElemBlock + int64_t(threadIdx.x) * 8;
+    if (idx >= kp * kp) return;
+    const float* A0 = reinterpret_cast<const float*>(w + WL.a32);
+    uint16_t* A = reinterpret_cast<uint16_t*>(w + WL.a);
+    const int64_t i = idx / kp, j = idx - i * kp;   // kp % 8 == 0: the 8 stay in row i
+    const float si = s[i];
+    uint16_t o[8];
 #pragma unroll
-  for (int e = 0; e < 8; ++e) o[e] = f2bf(A0[idx + e] * (si * s[j + e]));
-  *reinterpret_cast<uint4*>(A + idx) = *reinterpret_cast<const uint4*>(o);
+    for (int e = 0; e < 8; ++e) o[e] = f2bf(A0[idx + e] * (si * s[j + e]));
+    *reinterpret_cast<uint4*>(A + idx) = *reinterpret_cast<const uint4*>(o);
+    return;
+  }
+  const int64_t idx = int64_t(L.tile - nA) * kElemBlock + int64_t(threadIdx.x) * 8;
+  if (idx >= kp * Np) return;
+  uint16_t* Y = reinterpret_cast<uint16_t*>(w + WL.w1);
+  const float si = s[idx / Np];                    // Np % 8 == 0
+  uint4 v = *reinterpret_cast<const uint4*>(Y + idx);
+  uint16_t* e = reinterpret_cast<uint16_t*>(&v);
+#pragma unroll
+  for (int u = 0; u < 8; ++u) e[u] = f2bf(bf2f(e[u]) * si);
+  *reinterpret_cast<uint4*>(Y + idx) = v;
 }
 
 #define TM_LAUNCH(kern) \
@@ -537,12 +718,9 @@ __global__ __launch_bounds__(256) void k_scale_a(const Phase P) {
 
 template <int T>
 static hipError_t launch_t(int kind, const Phase& P, hipStream_t st) {
-  const bool scale = (P.flags & kScale) != 0u;
   switch (kind) {
     case kKindGram: TM_LAUNCH(k_gram_fast<T>);
-    case kKindPoly:
-      if (scale) TM_LAUNCH((k_poly_fast<T, true>));
-      TM_LAUNCH((k_poly_fast<T, false>));
+    case kKindPoly: TM_LAUNCH(k_poly_fast<T>);
     case kKindUpdate: TM_LAUNCH(k_update_fast<T>);
   }
   return hipErrorInvalidValue;
@@ -557,7 +735,7 @@ hipError_t launch_fast_bf16(int kind, int cfg, const Phase& P, hipStream_t st) {
     return hipGetLastError();
   }
   if (kind == kKindScaleA) {
-    hipLaunchKernelGGL(fast::k_scale_a, dim3(P.total), dim3(256), 0, st, P);
+    hipLaunchKernelGGL(fast::k_apply_s, dim3(P.total), dim3(256), 0, st, P);
     return hipGetLastError();
   }
   switch (cfg_tile(cfg)) {
