@@ -50,6 +50,9 @@ def main(argv=None) -> int:
     ap.add_argument("--precond", default="aol", choices=["aol", "frobenius", "none"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-check", action="store_true")
+    ap.add_argument("--copy-calibration-mb", type=int, default=0,
+                    help="after the timed region, run one plain device copy of this many MiB "
+                         "(reference kernel for scaling the FETCH_SIZE / WRITE_SIZE counters)")
     ap.add_argument("--inputs", default="powerlaw", choices=["powerlaw", "gaussian"],
                     help="powerlaw: the seeded power-law-plus-noise recipe (QR on the GPU); "
                          "gaussian: i.i.d. N(0,1) entries, the paper's own synthetic law "
@@ -172,8 +175,41 @@ def main(argv=None) -> int:
                                       "cores": cores, "kind": "oracle",
                                       "sample": f"1 of the {count} matrices ({m}x{n}), "
                                                 f"fp64 NumPy, {cpu_s:.2f} s"}
+    if args.copy_calibration_mb > 0:
+        nbytes = args.copy_calibration_mb << 20
+        src = torch.empty(nbytes // 2, dtype=torch.bfloat16, device=dev).fill_(1.0)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        result["copy_calibration_bytes"] = nbytes
+
+    traffic = _recorded_traffic(upd_flops_per_launch)
+    if traffic is not None:
+        result["roofline"]["traffic"] = traffic
     print(json.dumps(result), flush=True)
     return 0
+
+
+def _recorded_traffic(flops_per_launch):
+    """HBM bytes per k_update_fast launch from the committed counter summary.
+
+    The summary records the hash of the kernel source it was taken with; a
+    changed kernel reports null.
+    """
+    import hashlib
+    path = os.path.join(ROOT, "profiles", "k_update_fast_traffic.json")
+    src = os.path.join(ROOT, "paper_2512_04632_amd", "csrc", "tm_fast.hip")
+    try:
+        with open(path) as f:
+            rec = json.load(f)
+        with open(src, "rb") as f:
+            h = hashlib.sha256(f.read()).hexdigest()
+    except OSError:
+        return None
+    if rec.get("kernel_source_sha256") != h or rec.get("flops_per_launch") != flops_per_launch:
+        return None
+    return rec.get("hbm_bytes_per_launch")
 
 
 if __name__ == "__main__":
