@@ -18,8 +18,10 @@
 //                 diagonal, so the update is a single product with no second
 //                 read of Y
 //
-// Main loop: 256 threads = 4 wave64s in a 2 x 2 grid, each owning a
-// (T/2) x (T/2) block of 32 x 32 v_mfma_f32_32x32x16_bf16 accumulators.  K
+// Main loop: the 256 x 256 tile runs 8 wave64s (two per SIMD, so one wave's
+// barrier or DMA issue can hide behind the other's MFMAs) in a 2 x 4 grid of
+// 128 x 64 blocks; smaller tiles run 4 waves in a 2 x 2 grid.  Each wave
+// accumulates 32 x 32 v_mfma_f32_32x32x16_bf16 blocks.  K
 // advances 32 elements per stage through a 4-stage LDS ring filled by
 // global_load_lds_dwordx4 (direct to LDS, no VGPR staging), three stages in
 // flight.  K-contiguous operands are stored as 64-byte rows with the 16-byte
@@ -46,15 +48,20 @@ typedef short s16x4_t __attribute__((ext_vector_type(4)));
 constexpr int BK = 32;        // K elements per stage (64 bytes of a K-contiguous row)
 constexpr int STAGES = TM_FAST_STAGES;
 
+// Tile T x T computed by NW wave64s in a 2 x (NW/2) grid; each wave owns
+// (T/2) x (2T/NW) of the output as 32 x 32 MFMA blocks.
 template <int T>
 struct Tile {
-  static constexpr int TW = T / 2;              // wave tile
-  static constexpr int F = TW / 32;             // 32 x 32 blocks per wave side
+  static constexpr int NW = T == 256 ? 8 : 4;   // 2 waves per SIMD for the large tile
+  static constexpr int NT = 64 * NW;            // threads per workgroup
+  static constexpr int TWM = T / 2, TWN = 2 * T / NW;
+  static constexpr int FM = TWM / 32, FN = TWN / 32;
   static constexpr int A_BYTES = T * BK * 2;    // one operand stage
   static constexpr int STAGE = 2 * A_BYTES;
   static constexpr int LDS = STAGES * STAGE;
+  static constexpr int DMA_OP = T / 16 / NW;    // DMA instructions per wave per operand per stage
+  static constexpr int PER_STAGE = 2 * DMA_OP;
   static_assert(LDS <= 160 * 1024, "gfx950 LDS is 160 KB per workgroup");
-  static constexpr int PER_STAGE = T / 32;      // DMA instructions per wave per stage
 };
 
 __device__ inline float bf2f(uint16_t v) { return __uint_as_float(uint32_t(v) << 16); }
@@ -122,8 +129,8 @@ template <int T>
 __device__ inline void issue_kc(const uint16_t* src, int64_t ld, int k0, uint32_t lds) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
 #pragma unroll
-  for (int q = 0; q < T / 64; ++q) {
-    const int j = wave + 4 * q;
+  for (int q = 0; q < Tile<T>::DMA_OP; ++q) {
+    const int j = wave + Tile<T>::NW * q;
     const int r = j * 16 + (lane >> 2);
     const int c = (lane & 3) ^ ((r >> 2) & 3);
     const uint32_t voff = uint32_t((int64_t(r) * ld + k0 + c * 8) * 2);
@@ -145,8 +152,8 @@ __device__ inline void issue_rm(const uint16_t* src, int64_t ld, int k0, uint32_
   constexpr int RPI = 1024 / ROWB;        // rows per instruction
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
 #pragma unroll
-  for (int q = 0; q < T / 64; ++q) {
-    const int j = wave + 4 * q;
+  for (int q = 0; q < Tile<T>::DMA_OP; ++q) {
+    const int j = wave + Tile<T>::NW * q;
     const int r = j * RPI + lane / LPR;
     const int p16 = lane % LPR;
     const int c = (p16 >> 1) ^ swz_y<T>(r);
@@ -158,26 +165,26 @@ __device__ inline void issue_rm(const uint16_t* src, int64_t ld, int k0, uint32_
 // ---------------------------------------------------------------- compute
 template <int T>
 struct Frags {
-  uint4 a[Tile<T>::F], b[Tile<T>::F];
+  uint4 a[Tile<T>::FM], b[Tile<T>::FN];
 };
 
 // MFMA operands of K slice kk (16 wide) of one stage.
 template <int T, bool RM>
 __device__ inline void load_frags(Frags<T>& fr, const char* sa, const char* sb, int kk, int wm,
                                   int wn) {
-  constexpr int F = Tile<T>::F, TW = Tile<T>::TW;
+  constexpr int FM = Tile<T>::FM, FN = Tile<T>::FN;
   const int lane = threadIdx.x & 63;
   const int lr = lane & 31, lh = lane >> 5;
   const int c = 2 * kk + lh;
 #pragma unroll
-  for (int f = 0; f < F; ++f) {
-    const int r = wm * TW + f * 32 + lr;
+  for (int f = 0; f < FM; ++f) {
+    const int r = wm * Tile<T>::TWM + f * 32 + lr;
     fr.a[f] = *reinterpret_cast<const uint4*>(sa + r * 64 + 16 * (c ^ ((r >> 2) & 3)));
   }
   if constexpr (!RM) {
 #pragma unroll
-    for (int f = 0; f < F; ++f) {
-      const int r = wn * TW + f * 32 + lr;
+    for (int f = 0; f < FN; ++f) {
+      const int r = wn * Tile<T>::TWN + f * 32 + lr;
       fr.b[f] = *reinterpret_cast<const uint4*>(sb + r * 64 + 16 * (c ^ ((r >> 2) & 3)));
     }
   } else {
@@ -186,8 +193,8 @@ __device__ inline void load_frags(Frags<T>& fr, const char* sa, const char* sb, 
     const int g = lane >> 4, q = lane & 15;
     const int kb = 16 * kk + 8 * (g >> 1) + (q >> 2);
 #pragma unroll
-    for (int f = 0; f < F; ++f) {
-      const int chunk = (wn * TW + f * 32) / 16 + (g & 1);
+    for (int f = 0; f < FN; ++f) {
+      const int chunk = (wn * Tile<T>::TWN + f * 32) / 16 + (g & 1);
       s16x4_t v[2];
 #pragma unroll
       for (int h = 0; h < 2; ++h) {
@@ -206,12 +213,11 @@ __device__ inline void load_frags(Frags<T>& fr, const char* sa, const char* sb, 
 // the operands the other way round, so acc[fm][fn] holds the transposed block:
 // each lane then owns 4 consecutive columns of one C row.
 template <int T, bool SWAP>
-__device__ inline void mma(f32x16_t (&acc)[Tile<T>::F][Tile<T>::F], const Frags<T>& fr) {
-  constexpr int F = Tile<T>::F;
+__device__ inline void mma(f32x16_t (&acc)[Tile<T>::FM][Tile<T>::FN], const Frags<T>& fr) {
 #pragma unroll
-  for (int fm = 0; fm < F; ++fm)
+  for (int fm = 0; fm < Tile<T>::FM; ++fm)
 #pragma unroll
-    for (int fn = 0; fn < F; ++fn) {
+    for (int fn = 0; fn < Tile<T>::FN; ++fn) {
       if constexpr (SWAP)
         acc[fm][fn] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
             __builtin_bit_cast(bf16x8_t, fr.b[fn]), __builtin_bit_cast(bf16x8_t, fr.a[fm]),
@@ -233,16 +239,16 @@ __device__ inline void mma(f32x16_t (&acc)[Tile<T>::F][Tile<T>::F], const Frags<
 // and every wave done reading stage kt), the DMA of stage kt+4 reuses stage
 // kt's buffer, and slice 0 of stage kt+1 is read while slice 1's MFMAs run.
 template <int T, bool RM, bool SWAP = false>
-__device__ inline void mainloop(f32x16_t (&acc)[Tile<T>::F][Tile<T>::F], char* smem,
+__device__ inline void mainloop(f32x16_t (&acc)[Tile<T>::FM][Tile<T>::FN], char* smem,
                                 const uint16_t* a, int64_t lda, const uint16_t* b, int64_t ldb,
                                 int K) {
-  constexpr int F = Tile<T>::F, PS = Tile<T>::PER_STAGE;
+  constexpr int PS = Tile<T>::PER_STAGE;
   const int wave = threadIdx.x >> 6;
-  const int wm = wave >> 1, wn = wave & 1;
+  const int wm = wave / (Tile<T>::NW / 2), wn = wave % (Tile<T>::NW / 2);
 #pragma unroll
-  for (int fm = 0; fm < F; ++fm)
+  for (int fm = 0; fm < Tile<T>::FM; ++fm)
 #pragma unroll
-    for (int fn = 0; fn < F; ++fn)
+    for (int fn = 0; fn < Tile<T>::FN; ++fn)
 #pragma unroll
       for (int v = 0; v < 16; ++v) acc[fm][fn][v] = 0.f;
 
@@ -333,12 +339,14 @@ __device__ inline void tri_tile(int t, int nb, int& I, int& J) {
 
 template <int T>
 __device__ inline int acc_row(int wm, int fm, int v) {
-  return wm * Tile<T>::TW + fm * 32 + 8 * (v >> 2) + 4 * ((threadIdx.x & 63) >> 5) + (v & 3);
+  return wm * Tile<T>::TWM + fm * 32 + 8 * (v >> 2) + 4 * ((threadIdx.x & 63) >> 5) + (v & 3);
 }
 template <int T>
 __device__ inline int acc_col(int wn, int fn) {
-  return wn * Tile<T>::TW + fn * 32 + (threadIdx.x & 31);
+  return wn * Tile<T>::TWN + fn * 32 + (threadIdx.x & 31);
 }
+__device__ inline int wave_m(int nw) { return int(threadIdx.x >> 6) / (nw / 2); }
+__device__ inline int wave_n(int nw) { return int(threadIdx.x >> 6) % (nw / 2); }
 
 // ---------------------------------------------------------------- epilogues
 // Output tiles are staged through LDS (the ring is free after the main loop)
@@ -349,7 +357,7 @@ struct Stage {
   static constexpr int RS = (T + 8) * 2;            // padded row stride in bytes
   static constexpr int BYTES = T * RS;
   static constexpr int CPR = T / 8;                 // 16-byte chunks per row
-  static constexpr int PER_THREAD = T * CPR / 256;  // chunks per thread
+  static constexpr int PER_THREAD = T * CPR / Tile<T>::NT;  // chunks per thread
 };
 
 template <int T>
@@ -363,7 +371,7 @@ __device__ inline void store_rows(const char* st, uint16_t* dst, int64_t ld, int
                                   int64_t col0) {
 #pragma unroll 4
   for (int it = 0; it < Stage<T>::PER_THREAD; ++it) {
-    const int q = it * 256 + int(threadIdx.x);
+    const int q = it * Tile<T>::NT + int(threadIdx.x);
     const int r = q / Stage<T>::CPR, c8 = q % Stage<T>::CPR;
     const uint4 v = *reinterpret_cast<const uint4*>(st + r * Stage<T>::RS + c8 * 16);
     *reinterpret_cast<uint4*>(dst + (row0 + r) * ld + col0 + c8 * 8) = v;
@@ -376,7 +384,7 @@ __device__ inline void store_cols(const char* st, uint16_t* dst, int64_t ld, int
                                   int64_t col0) {
 #pragma unroll 2
   for (int it = 0; it < Stage<T>::PER_THREAD; ++it) {
-    const int q = it * 256 + int(threadIdx.x);
+    const int q = it * Tile<T>::NT + int(threadIdx.x);
     const int c = q / Stage<T>::CPR, r8 = q % Stage<T>::CPR;
     uint16_t v[8];
 #pragma unroll
@@ -394,7 +402,7 @@ __device__ inline void store_rows_user(const char* st, uint16_t* dst, int k, int
   const bool vec = (N % 8) == 0 && (reinterpret_cast<uintptr_t>(dst) & 15u) == 0u;
 #pragma unroll 2
   for (int it = 0; it < Stage<T>::PER_THREAD; ++it) {
-    const int q = it * 256 + int(threadIdx.x);
+    const int q = it * Tile<T>::NT + int(threadIdx.x);
     const int r = q / Stage<T>::CPR, c8 = q % Stage<T>::CPR;
     const int i = row0 + r, l = col0 + c8 * 8;
     if (i >= k || l >= N) continue;
@@ -416,7 +424,7 @@ __device__ inline void store_cols_user(const char* st, uint16_t* dst, int k, int
   const bool vec = (k % 8) == 0 && (reinterpret_cast<uintptr_t>(dst) & 15u) == 0u;
 #pragma unroll 2
   for (int it = 0; it < Stage<T>::PER_THREAD; ++it) {
-    const int q = it * 256 + int(threadIdx.x);
+    const int q = it * Tile<T>::NT + int(threadIdx.x);
     const int c = q / Stage<T>::CPR, r8 = q % Stage<T>::CPR;
     const int l = col0 + c, i = row0 + r8 * 8;
     if (l >= N || i >= k) continue;
@@ -439,7 +447,7 @@ __device__ inline void load_rows(char* st, const uint16_t* src, int64_t ld, int6
                                  int64_t col0) {
 #pragma unroll 4
   for (int it = 0; it < Stage<T>::PER_THREAD; ++it) {
-    const int q = it * 256 + int(threadIdx.x);
+    const int q = it * Tile<T>::NT + int(threadIdx.x);
     const int r = q / Stage<T>::CPR, c8 = q % Stage<T>::CPR;
     *reinterpret_cast<uint4*>(st + r * Stage<T>::RS + c8 * 16) =
         *reinterpret_cast<const uint4*>(src + (row0 + r) * ld + col0 + c8 * 8);
@@ -452,15 +460,13 @@ __device__ inline void load_rows(char* st, const uint16_t* src, int64_t ld, int6
 // off the diagonal, transposed as tile (I, J).  `staged` is the stage's
 // previous bf16 at that position (the polynomial preloads A's tile (J, I)).
 template <int T, class Fv>
-__device__ inline void epilogue_sym(const f32x16_t (&acc)[Tile<T>::F][Tile<T>::F], char* st,
+__device__ inline void epilogue_sym(const f32x16_t (&acc)[Tile<T>::FM][Tile<T>::FN], char* st,
                                     uint16_t* D, int64_t ld, int I, int J, Fv f) {
-  constexpr int F = Tile<T>::F;
-  const int wave = threadIdx.x >> 6;
-  const int wm = wave >> 1, wn = wave & 1;
+  const int wm = wave_m(Tile<T>::NW), wn = wave_n(Tile<T>::NW);
 #pragma unroll
-  for (int fm = 0; fm < F; ++fm)
+  for (int fm = 0; fm < Tile<T>::FM; ++fm)
 #pragma unroll
-    for (int fn = 0; fn < F; ++fn) {
+    for (int fn = 0; fn < Tile<T>::FN; ++fn) {
       const int c = acc_col<T>(wn, fn);
 #pragma unroll
       for (int v4 = 0; v4 < 4; ++v4) {
@@ -482,15 +488,13 @@ __device__ inline void epilogue_sym(const f32x16_t (&acc)[Tile<T>::F][Tile<T>::F
 // fp32 store of a symmetric tile and its mirror straight from the registers
 // (first Gram only).
 template <int T>
-__device__ inline void store_sym_f32(const f32x16_t (&acc)[Tile<T>::F][Tile<T>::F], float* D,
+__device__ inline void store_sym_f32(const f32x16_t (&acc)[Tile<T>::FM][Tile<T>::FN], float* D,
                                      int64_t ld, int I, int J) {
-  constexpr int F = Tile<T>::F;
-  const int wave = threadIdx.x >> 6;
-  const int wm = wave >> 1, wn = wave & 1;
+  const int wm = wave_m(Tile<T>::NW), wn = wave_n(Tile<T>::NW);
 #pragma unroll
-  for (int fm = 0; fm < F; ++fm)
+  for (int fm = 0; fm < Tile<T>::FM; ++fm)
 #pragma unroll
-    for (int fn = 0; fn < F; ++fn) {
+    for (int fn = 0; fn < Tile<T>::FN; ++fn) {
       const int j = J * T + acc_col<T>(wn, fn);
 #pragma unroll
       for (int v4 = 0; v4 < 4; ++v4) {
@@ -508,16 +512,16 @@ __device__ inline void store_sym_f32(const f32x16_t (&acc)[Tile<T>::F][Tile<T>::
 
 // ---------------------------------------------------------------- kernels
 template <int T>
-__global__ __launch_bounds__(256) void k_gram_fast(const Phase P) {
+__global__ __launch_bounds__(Tile<T>::NT) void k_gram_fast(const Phase P) {
   __shared__ __attribute__((aligned(1024))) char smem[smem_bytes<T>()];
-  constexpr int F = Tile<T>::F;
+  constexpr int FM = Tile<T>::FM, FN = Tile<T>::FN;
   const Loc L = locate(P, xcd_remap(blockIdx.x, P.total));
   const Entry& E = P.e[L.ent];
   const int kp = int(E.kp), Np = int(E.Np);
   int I, J;
   tri_tile(L.tile, kp / T, I, J);
   const uint16_t* Y = wbuf(P, E, L.mat, P.src);
-  f32x16_t acc[F][F];
+  f32x16_t acc[FM][FN];
   mainloop<T, false>(acc, smem, Y + int64_t(I) * T * Np, Np, Y + int64_t(J) * T * Np, Np, Np);
 
   char* w = ws_of(P, E, L.mat);
@@ -533,34 +537,38 @@ __global__ __launch_bounds__(256) void k_gram_fast(const Phase P) {
     // part[Jb][i] = sum over column block Jb of |A0_ij|, from the fp32 accumulators
     __syncthreads();
     float* part = reinterpret_cast<float*>(w + WL.part);
-    float* rs = reinterpret_cast<float*>(smem);       // [2][T] row sums per wn
-    float* cs = rs + 2 * T;                           // [2][T] column sums per wm
-    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-    const int wm = wave >> 1, wn = wave & 1;
+    constexpr int NWN = Tile<T>::NW / 2;
+    float* rs = reinterpret_cast<float*>(smem);       // [NW/2][T] row sums per wn
+    float* cs = rs + NWN * T;                         // [2][T] column sums per wm
+    const int lane = threadIdx.x & 63;
+    const int wm = wave_m(Tile<T>::NW), wn = wave_n(Tile<T>::NW);
 #pragma unroll
-    for (int fm = 0; fm < F; ++fm)
+    for (int fm = 0; fm < FM; ++fm)
 #pragma unroll
       for (int v = 0; v < 16; ++v) {
         float x = 0.f;
 #pragma unroll
-        for (int fn = 0; fn < F; ++fn) x += fabsf(acc[fm][fn][v]);
+        for (int fn = 0; fn < FN; ++fn) x += fabsf(acc[fm][fn][v]);
 #pragma unroll
         for (int off = 16; off >= 1; off >>= 1) x += __shfl_xor(x, off, 64);
         if ((lane & 31) == 0) rs[wn * T + acc_row<T>(wm, fm, v)] = x;
       }
 #pragma unroll
-    for (int fn = 0; fn < F; ++fn) {
+    for (int fn = 0; fn < FN; ++fn) {
       float x = 0.f;
 #pragma unroll
-      for (int fm = 0; fm < F; ++fm)
+      for (int fm = 0; fm < FM; ++fm)
 #pragma unroll
         for (int v = 0; v < 16; ++v) x += fabsf(acc[fm][fn][v]);
       x += __shfl_xor(x, 32, 64);
       if (lane < 32) cs[wm * T + acc_col<T>(wn, fn)] = x;
     }
     __syncthreads();
-    for (int r = threadIdx.x; r < T; r += 256) {
-      part[int64_t(J) * kp + I * T + r] = rs[r] + rs[T + r];
+    for (int r = threadIdx.x; r < T; r += Tile<T>::NT) {
+      float x = 0.f;
+#pragma unroll
+      for (int q = 0; q < NWN; ++q) x += rs[q * T + r];
+      part[int64_t(J) * kp + I * T + r] = x;
       if (I != J) part[int64_t(I) * kp + J * T + r] = cs[r] + cs[T + r];
     }
   }
@@ -569,9 +577,9 @@ __global__ __launch_bounds__(256) void k_gram_fast(const Phase P) {
 // B~ = b A + c A A + a I (upper tiles, mirrored).  The stage is preloaded with
 // A's tile (J, I), whose element (j, i) equals A_ij.
 template <int T>
-__global__ __launch_bounds__(256) void k_poly_fast(const Phase P) {
+__global__ __launch_bounds__(Tile<T>::NT) void k_poly_fast(const Phase P) {
   __shared__ __attribute__((aligned(1024))) char smem[smem_bytes<T>()];
-  constexpr int F = Tile<T>::F;
+  constexpr int FM = Tile<T>::FM, FN = Tile<T>::FN;
   const Loc L = locate(P, xcd_remap(blockIdx.x, P.total));
   const Entry& E = P.e[L.ent];
   const int kp = int(E.kp);
@@ -581,7 +589,7 @@ __global__ __launch_bounds__(256) void k_poly_fast(const Phase P) {
   const WsLayout WL = ws_layout(E.kp, E.Np, 2);
   const uint16_t* A = reinterpret_cast<const uint16_t*>(w + WL.a);
   uint16_t* B = reinterpret_cast<uint16_t*>(w + WL.b);
-  f32x16_t acc[F][F];
+  f32x16_t acc[FM][FN];
   mainloop<T, false>(acc, smem, A + int64_t(I) * T * kp, kp, A + int64_t(J) * T * kp, kp, kp);
   load_rows<T>(smem, A, kp, int64_t(J) * T, int64_t(I) * T);
   __syncthreads();
@@ -598,9 +606,9 @@ __global__ __launch_bounds__(256) void k_poly_fast(const Phase P) {
 // dst = kSlotFinal writes the caller's matrix (tall: transposed), otherwise
 // the workspace slot.
 template <int T>
-__global__ __launch_bounds__(256) void k_update_fast(const Phase P) {
+__global__ __launch_bounds__(Tile<T>::NT) void k_update_fast(const Phase P) {
   __shared__ __attribute__((aligned(1024))) char smem[smem_bytes<T>()];
-  constexpr int F = Tile<T>::F;
+  constexpr int FM = Tile<T>::FM, FN = Tile<T>::FN;
   const Loc L = locate(P, xcd_remap(blockIdx.x, P.total));
   const Entry& E = P.e[L.ent];
   const int kp = int(E.kp), Np = int(E.Np), k = int(E.k), N = int(E.N);
@@ -618,21 +626,21 @@ __global__ __launch_bounds__(256) void k_update_fast(const Phase P) {
   const WsLayout WL = ws_layout(E.kp, E.Np, 2);
   const uint16_t* B = reinterpret_cast<const uint16_t*>(w + WL.b);
   const uint16_t* Y = wbuf(P, E, L.mat, P.src);
-  f32x16_t acc[F][F];
+  f32x16_t acc[FM][FN];
   mainloop<T, true, true>(acc, smem, B + int64_t(I) * T * kp, kp, Y + int64_t(Lb) * T, Np, kp);
 
-  // acc[fm][fn] element v: output row i = wm*TW + fm*32 + lane%32, columns
-  // l0..l0+3 with l0 = wn*TW + fn*32 + 8(v/4) + 4(lane/32)
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  const int wm = wave >> 1, wn = wave & 1;
+  // acc[fm][fn] element v: output row i = wm*TWM + fm*32 + lane%32, columns
+  // l0..l0+3 with l0 = wn*TWN + fn*32 + 8(v/4) + 4(lane/32)
+  const int lane = threadIdx.x & 63;
+  const int wm = wave_m(Tile<T>::NW), wn = wave_n(Tile<T>::NW);
 #pragma unroll
-  for (int fm = 0; fm < F; ++fm)
+  for (int fm = 0; fm < FM; ++fm)
 #pragma unroll
-    for (int fn = 0; fn < F; ++fn) {
-      const int i = wm * Tile<T>::TW + fm * 32 + (lane & 31);
+    for (int fn = 0; fn < FN; ++fn) {
+      const int i = wm * Tile<T>::TWM + fm * 32 + (lane & 31);
 #pragma unroll
       for (int v4 = 0; v4 < 4; ++v4) {
-        const int l0 = wn * Tile<T>::TW + fn * 32 + 8 * v4 + 4 * (lane >> 5);
+        const int l0 = wn * Tile<T>::TWN + fn * 32 + 8 * v4 + 4 * (lane >> 5);
         uint16_t out[4];
 #pragma unroll
         for (int u = 0; u < 4; ++u) out[u] = f2bf(acc[fm][fn][4 * v4 + u]);
@@ -714,7 +722,7 @@ __global__ __launch_bounds__(256) void k_apply_s(const Phase P) {
 }
 
 #define TM_LAUNCH(kern) \
-  do { hipLaunchKernelGGL(kern, dim3(P.total), dim3(256), 0, st, P); return hipGetLastError(); } while (0)
+  do { hipLaunchKernelGGL(kern, dim3(P.total), dim3(Tile<T>::NT), 0, st, P); return hipGetLastError(); } while (0)
 
 template <int T>
 static hipError_t launch_t(int kind, const Phase& P, hipStream_t st) {
