@@ -116,10 +116,36 @@ __device__ inline void ring_sync() {
 template <int PS>
 __device__ inline void ring_wait(int stages) {
   __builtin_amdgcn_s_waitcnt(0xC07F);   // lgkmcnt(0), vmcnt/expcnt untouched
-  if (stages >= 3) ring_sync_dma<3 * PS>();
+  if (stages >= 4) ring_sync_dma<4 * PS>();
+  else if (stages == 3) ring_sync_dma<3 * PS>();
   else if (stages == 2) ring_sync_dma<2 * PS>();
   else if (stages == 1) ring_sync_dma<PS>();
   else ring_sync_dma<0>();
+}
+
+// DMA-only wait (no barrier): at most PENDING DMA instructions of this wave
+// still in flight.
+template <int PENDING>
+__device__ inline void dma_wait() {
+  if constexpr (PENDING == 0) asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  else if constexpr (PENDING == 4) asm volatile("s_waitcnt vmcnt(4)" ::: "memory");
+  else if constexpr (PENDING == 8) asm volatile("s_waitcnt vmcnt(8)" ::: "memory");
+  else if constexpr (PENDING == 12) asm volatile("s_waitcnt vmcnt(12)" ::: "memory");
+  else static_assert(PENDING == 0, "unsupported in-flight count");
+}
+
+template <int PS>
+__device__ inline void dma_wait_stages(int stages) {
+  if (stages >= 3) dma_wait<3 * PS>();
+  else if (stages == 2) dma_wait<2 * PS>();
+  else if (stages == 1) dma_wait<PS>();
+  else dma_wait<0>();
+}
+
+__device__ inline void barrier_pinned() {
+  __builtin_amdgcn_sched_barrier(0);
+  asm volatile("s_barrier" ::: "memory");
+  __builtin_amdgcn_sched_barrier(0);
 }
 
 // ---------------------------------------------------------------- DMA issue
@@ -287,6 +313,87 @@ __device__ inline void mainloop(f32x16_t (&acc)[Tile<T>::FM][Tile<T>::FN], char*
     mma<T, SWAP>(acc, f1);
   }
   ring_sync<0>();   // the ring is free for the epilogue
+}
+
+// Ping-pong schedule for the 8-wave tile.  Waves 0-3 (group 0) and 4-7
+// (group 1) occupy one slot per SIMD each; group 1 runs one phase behind, so
+// that while one wave of a SIMD issues the 16 MFMAs of a K step from
+// registers, the other issues its DMA and reads its operands of the next
+// step from LDS.  Every phase ends with a workgroup barrier:
+//   group 0: [MEM(j) | COMP(j)] for j = 0..nk-1, then one idle phase;
+//   group 1: one idle phase, then [MEM(j) | COMP(j)].
+// MEM(j) issues the DMA of stage j+S-1 (its buffer held stage j-1, whose
+// last reader, group 1's MEM(j-1), ended one barrier earlier) and reads
+// stage j.  Stage j+1 must be in LDS before group 0's MEM(j+1): group 0 waits
+// for its own DMA of that stage at the end of COMP(j), group 1 at the end of
+// MEM(j) (together with its LDS reads, so that stage j's buffer is free when
+// the next DMA into it is issued), both before the same barrier.
+template <int T, bool RM, bool SWAP>
+__device__ inline void mainloop_pp(f32x16_t (&acc)[Tile<T>::FM][Tile<T>::FN], char* smem,
+                                   const uint16_t* a, int64_t lda, const uint16_t* b,
+                                   int64_t ldb, int K) {
+  static_assert(Tile<T>::NW == 8, "ping-pong needs two waves per SIMD");
+  constexpr int PS = Tile<T>::PER_STAGE;
+  const int wave = threadIdx.x >> 6;
+  const int wm = wave / 4, wn = wave % 4;
+  const bool g1 = __builtin_amdgcn_readfirstlane(wave) >= 4;
+#pragma unroll
+  for (int fm = 0; fm < Tile<T>::FM; ++fm)
+#pragma unroll
+    for (int fn = 0; fn < Tile<T>::FN; ++fn)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) acc[fm][fn][v] = 0.f;
+
+  const uint32_t lds0 = lds_addr(smem);
+  const int nk = K / BK;
+  auto issue = [&](int kt) {
+    const uint32_t st = lds0 + uint32_t((kt % STAGES) * Tile<T>::STAGE);
+    issue_kc<T>(a, lda, kt * BK, st);
+    if constexpr (RM) issue_rm<T>(b, ldb, kt * BK, st + Tile<T>::A_BYTES);
+    else issue_kc<T>(b, ldb, kt * BK, st + Tile<T>::A_BYTES);
+  };
+  auto stage_ptr = [&](int kt) { return smem + (kt % STAGES) * Tile<T>::STAGE; };
+#pragma unroll
+  for (int s = 0; s + 1 < STAGES; ++s)
+    if (s < nk) issue(s);
+  ring_wait<PS>(min(nk - 1, STAGES - 2));
+  if (g1) barrier_pinned();
+
+  Frags<T> f0, f1;
+  for (int j = 0; j < nk; ++j) {
+    // MEM(j)
+    if (j + STAGES - 1 < nk) issue(j + STAGES - 1);
+    const char* st = stage_ptr(j);
+    load_frags<T, RM>(f0, st, st + Tile<T>::A_BYTES, 0, wm, wn);
+    load_frags<T, RM>(f1, st, st + Tile<T>::A_BYTES, 1, wm, wn);
+    const int pend = min(nk - 1, j + STAGES - 1) - (j + 1);
+    if (g1) {
+      __builtin_amdgcn_s_waitcnt(0xC07F);   // lgkmcnt(0)
+      dma_wait_stages<PS>(pend);
+    }
+    barrier_pinned();
+    // COMP(j)
+    mma<T, SWAP>(acc, f0);
+    mma<T, SWAP>(acc, f1);
+    if (!g1) dma_wait_stages<PS>(pend);
+    barrier_pinned();
+  }
+  if (!g1) barrier_pinned();
+  __builtin_amdgcn_s_waitcnt(0xC07F);
+  dma_wait<0>();   // nothing is in flight here; keeps the counter model exact
+}
+
+template <int T, bool RM, bool SWAP = false>
+__device__ inline void run_mainloop(f32x16_t (&acc)[Tile<T>::FM][Tile<T>::FN], char* smem,
+                                    const uint16_t* a, int64_t lda, const uint16_t* b,
+                                    int64_t ldb, int K) {
+#ifndef TM_NO_PINGPONG
+  if constexpr (Tile<T>::NW == 8) {
+    mainloop_pp<T, RM, SWAP>(acc, smem, a, lda, b, ldb, K);
+    return;
+  }
+#endif
+  mainloop<T, RM, SWAP>(acc, smem, a, lda, b, ldb, K);
 }
 
 // ---------------------------------------------------------------- mapping
@@ -522,7 +629,7 @@ __global__ __launch_bounds__(Tile<T>::NT) void k_gram_fast(const Phase P) {
   tri_tile(L.tile, kp / T, I, J);
   const uint16_t* Y = wbuf(P, E, L.mat, P.src);
   f32x16_t acc[FM][FN];
-  mainloop<T, false>(acc, smem, Y + int64_t(I) * T * Np, Np, Y + int64_t(J) * T * Np, Np, Np);
+  run_mainloop<T, false>(acc, smem, Y + int64_t(I) * T * Np, Np, Y + int64_t(J) * T * Np, Np, Np);
 
   char* w = ws_of(P, E, L.mat);
   const WsLayout WL = ws_layout(E.kp, E.Np, 2);
@@ -590,7 +697,7 @@ __global__ __launch_bounds__(Tile<T>::NT) void k_poly_fast(const Phase P) {
   const uint16_t* A = reinterpret_cast<const uint16_t*>(w + WL.a);
   uint16_t* B = reinterpret_cast<uint16_t*>(w + WL.b);
   f32x16_t acc[FM][FN];
-  mainloop<T, false>(acc, smem, A + int64_t(I) * T * kp, kp, A + int64_t(J) * T * kp, kp, kp);
+  run_mainloop<T, false>(acc, smem, A + int64_t(I) * T * kp, kp, A + int64_t(J) * T * kp, kp, kp);
   load_rows<T>(smem, A, kp, int64_t(J) * T, int64_t(I) * T);
   __syncthreads();
   const float a = P.a, b = P.b, c = P.c;
@@ -627,7 +734,7 @@ __global__ __launch_bounds__(Tile<T>::NT) void k_update_fast(const Phase P) {
   const uint16_t* B = reinterpret_cast<const uint16_t*>(w + WL.b);
   const uint16_t* Y = wbuf(P, E, L.mat, P.src);
   f32x16_t acc[FM][FN];
-  mainloop<T, true, true>(acc, smem, B + int64_t(I) * T * kp, kp, Y + int64_t(Lb) * T, Np, kp);
+  run_mainloop<T, true, true>(acc, smem, B + int64_t(I) * T * kp, kp, Y + int64_t(Lb) * T, Np, kp);
 
   // acc[fm][fn] element v: output row i = wm*TWM + fm*32 + lane%32, columns
   // l0..l0+3 with l0 = wn*TWN + fn*32 + 8(v/4) + 4(lane/32)
