@@ -397,10 +397,19 @@ __device__ inline void run_mainloop(f32x16_t (&acc)[Tile<T>::FM][Tile<T>::FN], c
 }
 
 // ---------------------------------------------------------------- mapping
+// Workgroup p runs on XCD p % 8 (round-robin dispatch).  Logical tiles are
+// dealt to the XCDs in chunks of 32 consecutive tiles: XCD x's j-th group of
+// 32 workgroups takes chunk 8 (j / 32) + x.  Neighbouring tiles (which share
+// operand rows) then run together on one XCD and hit its L2, while the eight
+// XCDs work on adjacent chunks of the same matrices, so operand panels that
+// leave one L2 are still in the memory-side cache when the next XCD asks for
+// them.  Workgroups past the last full round of 8 chunks keep their index.
 __device__ inline int xcd_remap(int p, int total) {
-  const int q = total >> 3, r = total & 7;
+  constexpr int C = 32;
+  const int full = total / (8 * C) * (8 * C);
+  if (p >= full) return p;
   const int x = p & 7, j = p >> 3;
-  return x * q + min(x, r) + j;
+  return ((j / C) * 8 + x) * C + (j % C);
 }
 
 struct Loc {
