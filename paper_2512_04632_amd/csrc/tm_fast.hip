@@ -362,19 +362,35 @@ __device__ inline void mainloop_pp(f32x16_t (&acc)[Tile<T>::FM][Tile<T>::FN], ch
   Frags<T> f0, f1;
   for (int j = 0; j < nk; ++j) {
     // MEM(j)
+#ifndef TM_PP_DMA_IN_COMP
     if (j + STAGES - 1 < nk) issue(j + STAGES - 1);
+    const int pend1 = min(nk - 1, j + STAGES - 1) - (j + 1);
+#else
+    const int pend1 = min(nk - 1, j + STAGES - 2) - (j + 1);
+#endif
     const char* st = stage_ptr(j);
     load_frags<T, RM>(f0, st, st + Tile<T>::A_BYTES, 0, wm, wn);
     load_frags<T, RM>(f1, st, st + Tile<T>::A_BYTES, 1, wm, wn);
     const int pend = min(nk - 1, j + STAGES - 1) - (j + 1);
     if (g1) {
       __builtin_amdgcn_s_waitcnt(0xC07F);   // lgkmcnt(0)
-      dma_wait_stages<PS>(pend);
+      dma_wait_stages<PS>(pend1);
     }
     barrier_pinned();
     // COMP(j)
+#ifdef TM_PP_SETPRIO
+    __builtin_amdgcn_s_setprio(1);
+#endif
     mma<T, SWAP>(acc, f0);
+#ifdef TM_PP_DMA_IN_COMP
+    __builtin_amdgcn_sched_barrier(0);
+    if (j + STAGES - 1 < nk) issue(j + STAGES - 1);
+    __builtin_amdgcn_sched_barrier(0);
+#endif
     mma<T, SWAP>(acc, f1);
+#ifdef TM_PP_SETPRIO
+    __builtin_amdgcn_s_setprio(0);
+#endif
     if (!g1) dma_wait_stages<PS>(pend);
     barrier_pinned();
   }
@@ -436,7 +452,7 @@ __device__ inline uint16_t* user_of(const Entry& E, int mat) {
   return reinterpret_cast<uint16_t*>(E.x + uint64_t(mat) * E.k * E.N * 2u);
 }
 
-// Workspace Y buffer of a slot (kp x Np, ld Np): the first slot is W1, then
+// Workspace Y buffer of a slot (kp x Np, ld ldy): the first slot is W1, then
 // W2, W1, ... (the final slot is the caller's matrix, handled by the update).
 __device__ inline uint16_t* wbuf(const Phase& P, const Entry& E, int mat, int slot) {
   const WsLayout L = ws_layout(E.kp, E.Np, 2);
@@ -495,19 +511,31 @@ __device__ inline void store_rows(const char* st, uint16_t* dst, int64_t ld, int
 }
 
 // Transposed: stage element (r, c) -> dst row row0 + c, column col0 + r.
+// Each 16-lane group moves an 8-row x 16-column block of the stage with two
+// ds_read_b64_tr_b16 (lane q addresses row 4h + q/4, columns 4(q%4).. of the
+// block and receives rows 4h..4h+3 of column q), then stores the 8 values of
+// its column as one 16-byte vector.  The four groups of a wave take adjacent
+// row blocks, so each destination row gets 64 contiguous bytes.
 template <int T>
 __device__ inline void store_cols(const char* st, uint16_t* dst, int64_t ld, int64_t row0,
                                   int64_t col0) {
+  constexpr int RB = T / 8;                      // 8-row blocks
+  constexpr int GROUPS = (T / 16) * RB;
+  constexpr int NG = Tile<T>::NT / 16;
+  static_assert(GROUPS % NG == 0, "whole passes");
+  const int q = threadIdx.x & 15;
 #pragma unroll 2
-  for (int it = 0; it < Stage<T>::PER_THREAD; ++it) {
-    const int q = it * Tile<T>::NT + int(threadIdx.x);
-    const int c = q / Stage<T>::CPR, r8 = q % Stage<T>::CPR;
-    uint16_t v[8];
+  for (int g = int(threadIdx.x) >> 4; g < GROUPS; g += NG) {
+    const int r8 = g % RB, cb = g / RB;
+    s16x4_t v[2];
 #pragma unroll
-    for (int e = 0; e < 8; ++e)
-      v[e] = *reinterpret_cast<const uint16_t*>(st + (r8 * 8 + e) * Stage<T>::RS + c * 2);
-    *reinterpret_cast<uint4*>(dst + (row0 + c) * ld + col0 + r8 * 8) =
-        *reinterpret_cast<const uint4*>(v);
+    for (int h = 0; h < 2; ++h) {
+      const char* p = st + (r8 * 8 + 4 * h + (q >> 2)) * Stage<T>::RS + (cb * 16 + 4 * (q & 3)) * 2;
+      v[h] = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+          (__attribute__((address_space(3))) s16x4_t*)(lds_addr(p)));
+    }
+    *reinterpret_cast<uint4*>(dst + (row0 + cb * 16 + q) * ld + col0 + r8 * 8) =
+        __builtin_bit_cast(uint4, v);
   }
 }
 
@@ -637,16 +665,17 @@ __global__ __launch_bounds__(Tile<T>::NT) void k_gram_fast(const Phase P) {
   int I, J;
   tri_tile(L.tile, kp / T, I, J);
   const uint16_t* Y = wbuf(P, E, L.mat, P.src);
-  f32x16_t acc[FM][FN];
-  run_mainloop<T, false>(acc, smem, Y + int64_t(I) * T * Np, Np, Y + int64_t(J) * T * Np, Np, Np);
-
   char* w = ws_of(P, E, L.mat);
   const WsLayout WL = ws_layout(E.kp, E.Np, 2);
+  const int64_t ldy = WL.ldy;
+  f32x16_t acc[FM][FN];
+  run_mainloop<T, false>(acc, smem, Y + int64_t(I) * T * ldy, ldy, Y + int64_t(J) * T * ldy, ldy, Np);
+
   if (P.flags & kA32) {
     store_sym_f32<T>(acc, reinterpret_cast<float*>(w + WL.a32), kp, I, J);
   } else {
     auto f = [](int, int, float x, uint16_t) { return x; };
-    epilogue_sym<T>(acc, smem, reinterpret_cast<uint16_t*>(w + WL.a), kp, I, J, f);
+    epilogue_sym<T>(acc, smem, reinterpret_cast<uint16_t*>(w + WL.a), WL.ldg, I, J, f);
   }
 
   if (P.flags & kRowSum) {
@@ -705,16 +734,17 @@ __global__ __launch_bounds__(Tile<T>::NT) void k_poly_fast(const Phase P) {
   const WsLayout WL = ws_layout(E.kp, E.Np, 2);
   const uint16_t* A = reinterpret_cast<const uint16_t*>(w + WL.a);
   uint16_t* B = reinterpret_cast<uint16_t*>(w + WL.b);
+  const int64_t ldg = WL.ldg;
   f32x16_t acc[FM][FN];
-  run_mainloop<T, false>(acc, smem, A + int64_t(I) * T * kp, kp, A + int64_t(J) * T * kp, kp, kp);
-  load_rows<T>(smem, A, kp, int64_t(J) * T, int64_t(I) * T);
+  run_mainloop<T, false>(acc, smem, A + int64_t(I) * T * ldg, ldg, A + int64_t(J) * T * ldg, ldg, kp);
+  load_rows<T>(smem, A, ldg, int64_t(J) * T, int64_t(I) * T);
   __syncthreads();
   const float a = P.a, b = P.b, c = P.c;
   const bool diag = I == J;
   auto f = [=](int i, int j, float x, uint16_t aij) {
     return b * bf2f(aij) + c * x + ((diag && i == j) ? a : 0.f);
   };
-  epilogue_sym<T>(acc, smem, B, kp, I, J, f);
+  epilogue_sym<T>(acc, smem, B, ldg, I, J, f);
 }
 
 // Y' = B~ Y.  The operands are fed transposed so that each lane holds 4
@@ -742,8 +772,9 @@ __global__ __launch_bounds__(Tile<T>::NT) void k_update_fast(const Phase P) {
   const WsLayout WL = ws_layout(E.kp, E.Np, 2);
   const uint16_t* B = reinterpret_cast<const uint16_t*>(w + WL.b);
   const uint16_t* Y = wbuf(P, E, L.mat, P.src);
+  const int64_t ldg = WL.ldg, ldy = WL.ldy;
   f32x16_t acc[FM][FN];
-  run_mainloop<T, true, true>(acc, smem, B + int64_t(I) * T * kp, kp, Y + int64_t(Lb) * T, Np, kp);
+  run_mainloop<T, true, true>(acc, smem, B + int64_t(I) * T * ldg, ldg, Y + int64_t(Lb) * T, ldy, kp);
 
   // acc[fm][fn] element v: output row i = wm*TWM + fm*32 + lane%32, columns
   // l0..l0+3 with l0 = wn*TWN + fn*32 + 8(v/4) + 4(lane/32)
@@ -765,7 +796,7 @@ __global__ __launch_bounds__(Tile<T>::NT) void k_update_fast(const Phase P) {
     }
   __syncthreads();
   if (P.dst != kSlotFinal)
-    store_rows<T>(smem, wbuf(P, E, L.mat, P.dst), Np, int64_t(I) * T, int64_t(Lb) * T);
+    store_rows<T>(smem, wbuf(P, E, L.mat, P.dst), ldy, int64_t(I) * T, int64_t(Lb) * T);
   else if ((E.flags & kTall) == 0u)
     store_rows_user<T>(smem, user_of(E, L.mat), k, N, I * T, Lb * T);
   else
@@ -773,18 +804,22 @@ __global__ __launch_bounds__(Tile<T>::NT) void k_update_fast(const Phase P) {
 }
 
 // W1 = X (wide) or X^T (tall) in the padded layout, zeros outside the matrix.
+// One block per 64 x 64 tile of W1.  Wide: each thread copies 8 consecutive
+// elements of two rows (16-byte loads where the row allows them); tall: the
+// tile goes through LDS to be transposed.
 __global__ __launch_bounds__(256) void k_load_in(const Phase P) {
   __shared__ uint16_t tile[kTransposeTile][kTransposeTile + 2];
   const Loc L = locate(P, blockIdx.x);
   const Entry& E = P.e[L.ent];
-  const int k = int(E.k), N = int(E.N), Np = int(E.Np);
+  const int k = int(E.k), N = int(E.N);
+  const int64_t ldy = ws_layout(E.kp, E.Np, 2).ldy;
   const int nI = int(E.kp) / kTransposeTile;
   const int ti = L.tile % nI, tl = L.tile / nI;
   const uint16_t* X = user_of(E, L.mat);
   uint16_t* W = wbuf(P, E, L.mat, kSlotFirst);
   const bool tall = (E.flags & kTall) != 0u;
-  const int c = threadIdx.x & 63, r0 = threadIdx.x >> 6;
   if (tall) {
+    const int c = threadIdx.x & 63, r0 = threadIdx.x >> 6;
     for (int r = r0; r < kTransposeTile; r += 4) {
       const int l = tl * kTransposeTile + r, i = ti * kTransposeTile + c;
       tile[r][c] = (l < N && i < k) ? X[int64_t(l) * k + i] : uint16_t(0);
@@ -792,12 +827,23 @@ __global__ __launch_bounds__(256) void k_load_in(const Phase P) {
     __syncthreads();
     for (int r = r0; r < kTransposeTile; r += 4) {
       const int i = ti * kTransposeTile + r, l = tl * kTransposeTile + c;
-      W[int64_t(i) * Np + l] = tile[c][r];
+      W[int64_t(i) * ldy + l] = tile[c][r];
     }
   } else {
-    for (int r = r0; r < kTransposeTile; r += 4) {
-      const int i = ti * kTransposeTile + r, l = tl * kTransposeTile + c;
-      W[int64_t(i) * Np + l] = (i < k && l < N) ? X[int64_t(i) * N + l] : uint16_t(0);
+    const bool vec = (N % 8) == 0 && (reinterpret_cast<uintptr_t>(X) & 15u) == 0u;
+    const int c8 = threadIdx.x & 7, r0 = threadIdx.x >> 3;
+    const int l = tl * kTransposeTile + c8 * 8;
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const int i = ti * kTransposeTile + r0 + 32 * h;
+      uint4 v = make_uint4(0u, 0u, 0u, 0u);
+      if (i < k && vec && l + 8 <= N) {
+        v = *reinterpret_cast<const uint4*>(X + int64_t(i) * N + l);
+      } else if (i < k) {
+        uint16_t* e = reinterpret_cast<uint16_t*>(&v);
+        for (int u = 0; u < 8; ++u) e[u] = l + u < N ? X[int64_t(i) * N + l + u] : uint16_t(0);
+      }
+      *reinterpret_cast<uint4*>(W + int64_t(i) * ldy + l) = v;
     }
   }
 }
@@ -823,18 +869,19 @@ __global__ __launch_bounds__(256) void k_apply_s(const Phase P) {
     uint16_t o[8];
 #pragma unroll
     for (int e = 0; e < 8; ++e) o[e] = f2bf(A0[idx + e] * (si * s[j + e]));
-    *reinterpret_cast<uint4*>(A + idx) = *reinterpret_cast<const uint4*>(o);
+    *reinterpret_cast<uint4*>(A + i * WL.ldg + j) = *reinterpret_cast<const uint4*>(o);
     return;
   }
   const int64_t idx = int64_t(L.tile - nA) * kElemBlock + int64_t(threadIdx.x) * 8;
   if (idx >= kp * Np) return;
-  uint16_t* Y = reinterpret_cast<uint16_t*>(w + WL.w1);
-  const float si = s[idx / Np];                    // Np % 8 == 0
-  uint4 v = *reinterpret_cast<const uint4*>(Y + idx);
+  const int64_t i = idx / Np, l = idx - i * Np;   // Np % 8 == 0: the 8 stay in row i
+  uint16_t* Y = reinterpret_cast<uint16_t*>(w + WL.w1) + i * WL.ldy + l;
+  const float si = s[i];
+  uint4 v = *reinterpret_cast<const uint4*>(Y);
   uint16_t* e = reinterpret_cast<uint16_t*>(&v);
 #pragma unroll
   for (int u = 0; u < 8; ++u) e[u] = f2bf(bf2f(e[u]) * si);
-  *reinterpret_cast<uint4*>(Y + idx) = v;
+  *reinterpret_cast<uint4*>(Y) = v;
 }
 
 #define TM_LAUNCH(kern) \

@@ -104,16 +104,19 @@ TM_HD uint32_t blocks_per_matrix(int kind, int cfg, uint32_t k, uint32_t N, uint
 
 struct WsLayout {
   uint64_t w1, w2, a, b, a32, s, part, fpart, total;
+  uint32_t ldy, ldg;   // row strides (elements) of the Y buffers and of A, B
 };
 
 // Byte offsets of the sub-buffers of one matrix's workspace region, for
-// padded dims kp x Np: Y buffers kp x Np (ld Np), A, B kp x kp (ld kp), the
-// fp32 first Gram kp x kp, s (kp floats), row-sum partials
-// [ceil(kp / 64)][kp] and the Frobenius partials.
+// padded dims kp x Np: Y buffers kp x Np (ld ldy = Np), A, B kp x kp (ld
+// ldg = kp), the fp32 first Gram kp x kp (ld kp), s (kp floats), row-sum
+// partials [ceil(kp / 64)][kp] and the Frobenius partials.
 TM_HD WsLayout ws_layout(uint32_t kp, uint32_t Np, uint32_t esz) {
   WsLayout L;
-  const uint64_t y = align256(uint64_t(kp) * Np * esz);
-  const uint64_t g = align256(uint64_t(kp) * kp * esz);
+  L.ldy = Np;
+  L.ldg = kp;
+  const uint64_t y = align256(uint64_t(kp) * L.ldy * esz);
+  const uint64_t g = align256(uint64_t(kp) * L.ldg * esz);
   L.w1 = 0;
   L.w2 = L.w1 + y;
   L.a = L.w2 + y;
