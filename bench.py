@@ -1,11 +1,12 @@
 """Throughput of Turbo-Muon orthogonalization (AOL + 4 quintic Newton-Schulz
 iterations) on one MI355X, through the C ABI of libturbomuon.so.
 
-One step = one tm_orthogonalize call over a batch of synthetic gradient-like
-matrices already resident in HBM (default: 8 bf16 4096 x 14336 matrices,
-power-law spectrum k^-0.5 plus 0.01 Gaussian noise).  The batch is updated in
-place, so step i+1 orthogonalizes the output of step i; the kernels' work does
-not depend on the values.  Prints one JSON line.
+One step = one library call over a workload of synthetic gradient-like
+matrices already resident in HBM (default: one batched tm_orthogonalize call
+on 8 bf16 4096 x 14336 matrices, power-law spectrum j^-0.5 plus 0.01 Gaussian
+noise; workloads with several shapes use one tm_orthogonalize_grouped call).
+The matrices are updated in place, so step i+1 orthogonalizes the output of
+step i; the kernels' work does not depend on the values.  Prints one JSON line.
 """
 from __future__ import annotations
 
@@ -23,12 +24,11 @@ PEAK_BF16_TFLOPS = 2500.0     # MI355X dense bf16 matrix-core peak (published)
 PEAK_F32_TFLOPS = 157.3
 HBM_GBPS = 8000.0
 
-WORKLOADS = {
-    # name: (count, m, n, alpha, dtype)
-    "llm8b_4096x14336_b8": (8, 4096, 14336, 0.5, "bf16"),
-    "llm8b_4096x4096_b8": (8, 4096, 4096, 0.5, "bf16"),
-    "gpt2_mlp_768x3072": (1, 768, 3072, 0.8, "bf16"),
-}
+# Workloads are the synthetic recipes of paper_2512_04632_amd.synth: a list of
+# (count, m, n, alpha) entries in one storage dtype.  One-entry workloads run as
+# one batched call, several entries as one grouped call.
+DEFAULT_WORKLOAD = "llm8b_4096x14336_b8"
+PRECOND_NAME = {"aol": "AOL", "frobenius": "Frobenius", "none": "no pre-conditioning"}
 
 
 def alg_flops(k: int, N: int, iters: int) -> dict:
@@ -45,7 +45,8 @@ def main(argv=None) -> int:
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--workload", default="llm8b_4096x14336_b8", choices=sorted(WORKLOADS))
+    ap.add_argument("--workload", default=DEFAULT_WORKLOAD,
+                    help="one of paper_2512_04632_amd.synth.WORKLOADS")
     ap.add_argument("--iters", type=int, default=4)
     ap.add_argument("--precond", default="aol", choices=["aol", "frobenius", "none"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -70,8 +71,15 @@ def main(argv=None) -> int:
     from paper_2512_04632_amd import _lib as tm
     from paper_2512_04632_amd import synth
 
-    count, m, n, alpha, dtype = WORKLOADS[args.workload]
-    k, N = min(m, n), max(m, n)
+    if args.workload not in synth.WORKLOADS:
+        print(f"bench.py: unknown workload {args.workload!r}; choose from "
+              f"{sorted(synth.WORKLOADS)}", file=sys.stderr)
+        return 2
+    spec = synth.WORKLOADS[args.workload]
+    dtype = spec["dtype"]
+    entries = spec["entries"]
+    tdtype = torch.bfloat16 if dtype == "bf16" else torch.float32
+    grouped = len(entries) > 1
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     stream = torch.cuda.current_stream(dev)
@@ -79,29 +87,40 @@ def main(argv=None) -> int:
     def progress(msg):
         print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
-    progress(f"generating {count} x {m}x{n} {dtype} alpha={alpha}")
-    if args.inputs == "powerlaw":
-        X = synth.power_law_batch_device(count, m, n, alpha, seed=0, device=dev)
-    else:
-        g = torch.Generator(device=dev)
-        g.manual_seed(0)
-        X = torch.randn((count, m, n), generator=g, device=dev, dtype=torch.float32).to(torch.bfloat16)
+    progress(f"generating {args.workload}: {entries} {dtype}")
+    batches = []
+    for e, (count, m, n, alpha) in enumerate(entries):
+        if args.inputs == "powerlaw":
+            X = synth.power_law_batch_device(count, m, n, alpha, seed=e, device=dev, dtype=tdtype)
+        else:
+            g = torch.Generator(device=dev)
+            g.manual_seed(e)
+            X = torch.randn((count, m, n), generator=g, device=dev, dtype=torch.float32).to(tdtype)
+        batches.append(X)
     torch.cuda.synchronize()
-    x0_host = X[0].float().cpu().numpy().astype(np.float64)   # oracle input (exact bf16 values)
+    n_mat = sum(c for c, _, _, _ in entries)
 
-    # One checked call from the pristine input: matrix 0 against the oracle.
-    check = {}
-    out0 = None
+    def run(bs):
+        if grouped:
+            tm.orthogonalize_grouped([X[i] for X in bs for i in range(X.shape[0])], args.iters,
+                                     None, args.precond)
+        else:
+            tm.orthogonalize(bs[0], args.iters, None, args.precond)
+
+    # One checked call from the pristine inputs: matrix 0 of every entry
+    # against the oracle, on the exact stored values.
+    hosts = [X[0].float().cpu().numpy().astype(np.float64) for X in batches]
+    outs = None
     if not args.no_check:
-        Xc = X[:1].clone()
-        tm.orthogonalize(Xc, args.iters, None, args.precond)
+        clones = [X.clone() for X in batches]
+        run(clones)
         torch.cuda.synchronize()
-        out0 = Xc[0].float().cpu().numpy().astype(np.float64)
-        del Xc
+        outs = [X[0].float().cpu().numpy().astype(np.float64) for X in clones]
+        del clones
 
     progress(f"warmup {args.warmup}")
     for _ in range(args.warmup):
-        tm.orthogonalize(X, args.iters, None, args.precond)
+        run(batches)
     torch.cuda.synchronize()
 
     tm.timing_reset()
@@ -110,26 +129,35 @@ def main(argv=None) -> int:
     torch.cuda.synchronize()
     start.record(stream)
     for _ in range(args.steps):
-        tm.orthogonalize(X, args.iters, None, args.precond)
+        run(batches)
     stop.record(stream)
     torch.cuda.synchronize()
     tm.timing_enable(False)
     elapsed_ms = start.elapsed_time(stop)
-    phases = {p: tm.timing_read(p) for p in ("gram", "aol_vector", "poly", "update", "frob")}
+    phase_names = ("load_in", "frob", "gram", "aol_vector", "scale_a", "poly", "update")
+    phases = {p: tm.timing_read(p) for p in phase_names}
     progress(f"timed {args.steps} steps: {elapsed_ms:.3f} ms")
 
     ms_per_step = elapsed_ms / args.steps
-    fl = alg_flops(k, N, args.iters)
-    step_flops = fl["total"] * count
+    step_flops = 0
+    upd_flops_per_launch = 0
+    for count, m, n, _ in entries:
+        fl = alg_flops(min(m, n), max(m, n), args.iters)
+        step_flops += fl["total"] * count
+        upd_flops_per_launch += fl["update_per_iter"] * count
     tflops = step_flops / (ms_per_step * 1e-3) / 1e12
     upd_ms, upd_n = phases["update"]
     upd_avg_ms = upd_ms / max(upd_n, 1)
-    upd_flops_per_launch = fl["update_per_iter"] * count
     upd_tflops = upd_flops_per_launch / (upd_avg_ms * 1e-3) / 1e12
+    peak = PEAK_BF16_TFLOPS if dtype == "bf16" else PEAK_F32_TFLOPS
 
+    config = {"workload": args.workload, "matrices": n_mat,
+              "shapes": [[c, m, n] for c, m, n, _ in entries],
+              "alpha": [a for _, _, _, a in entries], "iters": args.iters,
+              "precond": args.precond, "call": "grouped" if grouped else "batched"}
     result = {
-        "metric": "orthogonalized matrices/s (AOL + 4 NS iterations)",
-        "value": round(count * args.steps / (elapsed_ms * 1e-3), 3),
+        "metric": f"orthogonalized matrices/s ({PRECOND_NAME[args.precond]} + {args.iters} NS iterations)",
+        "value": round(n_mat * args.steps / (elapsed_ms * 1e-3), 3),
         "unit": "matrices/s",
         "n_gpus": 1,
         "steps": args.steps,
@@ -141,40 +169,54 @@ def main(argv=None) -> int:
         "dtype": dtype,
         "data": ("synthetic (seeded power-law spectrum + 0.01 Gaussian noise)"
                  if args.inputs == "powerlaw" else "synthetic (seeded i.i.d. N(0,1))"),
-        "config": {"workload": args.workload, "matrices": count, "m": m, "n": n,
-                   "alpha": alpha, "iters": args.iters, "precond": args.precond},
+        "config": config,
         "tflops_algorithmic": round(tflops, 2),
-        "pct_bf16_peak": round(100 * tflops / PEAK_BF16_TFLOPS, 2),
+        "pct_peak": round(100 * tflops / peak, 2),
         "phase_ms_per_step": {p: round(v[0] / args.steps, 4) for p, v in phases.items()},
         "roofline": {"bound": "mfma", "kernel": "k_update",
-                     "achieved": round(upd_tflops, 2), "peak": PEAK_BF16_TFLOPS,
-                     "unit": "TFLOP/s", "frac": round(upd_tflops / PEAK_BF16_TFLOPS, 4),
+                     "achieved": round(upd_tflops, 2), "peak": peak,
+                     "unit": "TFLOP/s", "frac": round(upd_tflops / peak, 4),
                      "traffic": None,
                      "launch_avg_ms": round(upd_avg_ms, 4),
                      "flops_per_launch": upd_flops_per_launch},
     }
 
-    if out0 is not None or not args.no_cpu_baseline:
+    if outs is not None or not args.no_cpu_baseline:
         from oracle import turbomuon as O
-        t0 = time.perf_counter()
-        ref0 = O.orthogonalize(x0_host, args.iters, None, args.precond)
-        cpu_s = time.perf_counter() - t0
-        if out0 is not None:
-            check = {"rel_frobenius_vs_oracle": float(O.rel_frobenius(out0, ref0)),
-                     "eps_ortho_gpu": float(O.eps_ortho(out0)),
-                     "eps_ortho_oracle": float(O.eps_ortho(ref0)),
-                     "matrix": 0}
-            result["parity"] = check
+        refs, cpu_s = [], []
+        for Xh in hosts:
+            t0 = time.perf_counter()
+            refs.append(O.orthogonalize(Xh, args.iters, None, args.precond))
+            cpu_s.append(time.perf_counter() - t0)
+        if outs is not None:
+            result["parity"] = [{"entry": e, "matrix": 0,
+                                 "rel_frobenius_vs_oracle": float(O.rel_frobenius(o, r)),
+                                 "eps_ortho_gpu": float(O.eps_ortho(o)),
+                                 "eps_ortho_oracle": float(O.eps_ortho(r))}
+                                for e, (o, r) in enumerate(zip(outs, refs))]
         if not args.no_cpu_baseline:
+            # Bounded sample: the oracle on the workload's matrices in order
+            # (the first matrix of each entry already timed above, then more of
+            # the first entry) until about 10 s of CPU time have been spent.
+            done, spent = len(hosts), sum(cpu_s)
+            X0 = batches[0]
+            i = 1
+            while spent < 10.0 and i < X0.shape[0]:
+                Xh = X0[i].float().cpu().numpy().astype(np.float64)
+                t0 = time.perf_counter()
+                O.orthogonalize(Xh, args.iters, None, args.precond)
+                spent += time.perf_counter() - t0
+                done += 1
+                i += 1
             try:
                 from threadpoolctl import threadpool_info
                 cores = max(int(i.get("num_threads", 1)) for i in threadpool_info()) or 1
             except Exception:  # noqa: BLE001
                 cores = os.cpu_count() or 1
-            result["cpu_baseline"] = {"value": round(1.0 / cpu_s, 5), "unit": "matrices/s",
-                                      "cores": cores, "kind": "oracle",
-                                      "sample": f"1 of the {count} matrices ({m}x{n}), "
-                                                f"fp64 NumPy, {cpu_s:.2f} s"}
+            result["cpu_baseline"] = {
+                "value": round(done / spent, 5), "unit": "matrices/s", "cores": cores,
+                "kind": "oracle",
+                "sample": f"{done} of the {n_mat} matrices, fp64 NumPy, {spent:.2f} s"}
     if args.copy_calibration_mb > 0:
         nbytes = args.copy_calibration_mb << 20
         src = torch.empty(nbytes // 2, dtype=torch.bfloat16, device=dev).fill_(1.0)
@@ -184,7 +226,7 @@ def main(argv=None) -> int:
         torch.cuda.synchronize()
         result["copy_calibration_bytes"] = nbytes
 
-    traffic = _recorded_traffic(upd_flops_per_launch)
+    traffic = _recorded_traffic(upd_flops_per_launch) if args.workload == DEFAULT_WORKLOAD else None
     if traffic is not None:
         result["roofline"]["traffic"] = traffic
     print(json.dumps(result), flush=True)

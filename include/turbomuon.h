@@ -128,7 +128,9 @@ tm_status tm_release_workspaces(void);
 #define TM_PHASE_UPDATE        5  /* X <- a X + B X */
 #define TM_PHASE_APPLY_SCALE   6  /* iters = 0: X1 = diag(s) X0 */
 #define TM_PHASE_COPY_OUT      7  /* iters = 1: result copied into the caller's buffer */
-#define TM_NUM_PHASES          8
+#define TM_PHASE_LOAD_IN       8  /* bf16: X (or X^T) copied into the zero-padded workspace */
+#define TM_PHASE_SCALE_A       9  /* bf16: A1 = diag(s) A0 diag(s) and X1 = diag(s) X0 */
+#define TM_NUM_PHASES         10
 
 /* Timing hooks (a profiling aid for benchmarks).  While enabled, every kernel
  * launch of later calls is bracketed by a pair of HIP events recorded on the

@@ -23,7 +23,7 @@ TM_ERR_HIP = -4
 
 PRECOND = {"none": 0, "frobenius": 1, "frob": 1, "aol": 2}
 PHASES = {"transpose_in": 0, "frob": 1, "gram": 2, "aol_vector": 3, "poly": 4, "update": 5,
-          "apply_scale": 6, "copy_out": 7}
+          "apply_scale": 6, "copy_out": 7, "load_in": 8, "scale_a": 9}
 TM_MAX_DIM = 65536
 TM_MAX_ITERS = 64
 

@@ -54,6 +54,7 @@ struct TimedLaunch {
 };
 bool g_timing = false;
 std::vector<TimedLaunch> g_timed;
+static_assert(int(tmk::kNumKinds) == TM_NUM_PHASES, "one timing phase per kernel kind");
 double g_time_ms[TM_NUM_PHASES];
 int64_t g_time_n[TM_NUM_PHASES];
 
@@ -159,6 +160,22 @@ int choose_tile_cfg(const std::vector<Item>& items) {
   return tmk::kNumCfg - 1;
 }
 
+// bf16 Gram and polynomial phases: the layout tile T (kp, Np multiples of
+// it) is halved, down to 64, while the phase has fewer than two waves of
+// tiles for the 256 compute units; these phases have about k^2 / T^2 / 2
+// tiles per matrix against k N / T^2 for the update.
+int choose_sym_cfg(int kind, int tcfg, const std::vector<Item>& items) {
+  int cfg = tcfg;
+  while (cfg < tmk::kNumCfg - 1) {
+    uint64_t tiles = 0;
+    for (const Item& it : items)
+      tiles += uint64_t(it.count) * tmk::blocks_per_matrix(kind, cfg, it.k, it.N, it.kp, it.Np);
+    if (tiles >= 512) break;
+    ++cfg;
+  }
+  return cfg;
+}
+
 struct Plan {
   const std::vector<Item>* items;
   std::vector<uint64_t> ws_off;   // byte offset of each item's workspace region
@@ -231,7 +248,9 @@ tm_status launch(const Plan& pl, int kind, int cfg, int src, int dst, float a, f
 // bf16: zero-padded tiled workspace, matrix-core kernels of tm_fast.hip.
 tm_status plan_bf16(const Plan& pl, int iters, const float* coeffs, int precond, int tcfg) {
   const bool aol = precond == TM_PRECOND_AOL, frob = precond == TM_PRECOND_FROBENIUS;
-  const int T = tmk::cfg_tile(tcfg);
+  const int gcfg = choose_sym_cfg(tmk::kKindGram, tcfg, *pl.items);
+  const int pcfg = choose_sym_cfg(tmk::kKindPoly, tcfg, *pl.items);
+  const int T = tmk::kMinTile;   // the matrix-core Gram emits row sums per 64 columns
   tm_status s = TM_OK;
   if (iters > 0 || aol) s = launch(pl, tmk::kKindLoadIn, 0, 0, 0, 0.f, 0.f, 0.f, 0u, 0, false);
   if (s == TM_OK && frob) {  // Algorithm 1, first line: s = 1 / ||X0||_F
@@ -241,7 +260,7 @@ tm_status plan_bf16(const Plan& pl, int iters, const float* coeffs, int precond,
   if (s != TM_OK) return s;
   if (iters == 0) {
     if (aol) {
-      s = launch(pl, tmk::kKindGram, tcfg, tmk::kSlotFirst, 0, 0.f, 0.f, 0.f,
+      s = launch(pl, tmk::kKindGram, gcfg, tmk::kSlotFirst, 0, 0.f, 0.f, 0.f,
                  tmk::kRowSum | tmk::kA32, 0, false);
       if (s == TM_OK) s = launch(pl, tmk::kKindAolVector, 0, 0, 0, 0.f, 0.f, 0.f, 0u, T, false);
       if (s != TM_OK) return s;
@@ -258,12 +277,12 @@ tm_status plan_bf16(const Plan& pl, int iters, const float* coeffs, int precond,
     const bool first = it == 1;
     const uint32_t scale = (first && (aol || frob)) ? tmk::kScale : 0u;
     const uint32_t gflags = ((first && aol) ? tmk::kRowSum : 0u) | (scale ? tmk::kA32 : 0u);
-    s = launch(pl, tmk::kKindGram, tcfg, src, 0, 0.f, 0.f, 0.f, gflags, 0, false);
+    s = launch(pl, tmk::kKindGram, gcfg, src, 0, 0.f, 0.f, 0.f, gflags, 0, false);
     if (s == TM_OK && first && aol)  // Algorithm 2, second line: the AOL vector
       s = launch(pl, tmk::kKindAolVector, 0, 0, 0, 0.f, 0.f, 0.f, 0u, T, false);
     if (s == TM_OK && scale)         // A1 = diag(s) A0 diag(s), one rounding
       s = launch(pl, tmk::kKindScaleA, 0, 0, 0, 0.f, 0.f, 0.f, 0u, 0, false);
-    if (s == TM_OK) s = launch(pl, tmk::kKindPoly, tcfg, 0, 0, a, b, c, scale, 0, false);
+    if (s == TM_OK) s = launch(pl, tmk::kKindPoly, pcfg, 0, 0, a, b, c, scale, 0, false);
     if (s == TM_OK) s = launch(pl, tmk::kKindUpdate, tcfg, src, dst, a, b, c, scale, 0, false);
     src = dst;
   }

@@ -362,35 +362,19 @@ __device__ inline void mainloop_pp(f32x16_t (&acc)[Tile<T>::FM][Tile<T>::FN], ch
   Frags<T> f0, f1;
   for (int j = 0; j < nk; ++j) {
     // MEM(j)
-#ifndef TM_PP_DMA_IN_COMP
     if (j + STAGES - 1 < nk) issue(j + STAGES - 1);
-    const int pend1 = min(nk - 1, j + STAGES - 1) - (j + 1);
-#else
-    const int pend1 = min(nk - 1, j + STAGES - 2) - (j + 1);
-#endif
     const char* st = stage_ptr(j);
     load_frags<T, RM>(f0, st, st + Tile<T>::A_BYTES, 0, wm, wn);
     load_frags<T, RM>(f1, st, st + Tile<T>::A_BYTES, 1, wm, wn);
     const int pend = min(nk - 1, j + STAGES - 1) - (j + 1);
     if (g1) {
       __builtin_amdgcn_s_waitcnt(0xC07F);   // lgkmcnt(0)
-      dma_wait_stages<PS>(pend1);
+      dma_wait_stages<PS>(pend);
     }
     barrier_pinned();
     // COMP(j)
-#ifdef TM_PP_SETPRIO
-    __builtin_amdgcn_s_setprio(1);
-#endif
     mma<T, SWAP>(acc, f0);
-#ifdef TM_PP_DMA_IN_COMP
-    __builtin_amdgcn_sched_barrier(0);
-    if (j + STAGES - 1 < nk) issue(j + STAGES - 1);
-    __builtin_amdgcn_sched_barrier(0);
-#endif
     mma<T, SWAP>(acc, f1);
-#ifdef TM_PP_SETPRIO
-    __builtin_amdgcn_s_setprio(0);
-#endif
     if (!g1) dma_wait_stages<PS>(pend);
     barrier_pinned();
   }
@@ -433,8 +417,14 @@ struct Loc {
 };
 
 __device__ inline Loc locate(const Phase& P, int lid) {
-  int e = 0;
-  while (e + 1 < P.nent && lid >= int(P.e[e + 1].tile_start)) ++e;
+  // last entry whose first block is <= lid (entries without blocks share the
+  // start of the next entry and are never the last such entry)
+  int e = 0, hi = P.nent - 1;
+  while (e < hi) {
+    const int mid = (e + hi + 1) >> 1;
+    if (lid >= int(P.e[mid].tile_start)) e = mid;
+    else hi = mid - 1;
+  }
   const int r = lid - int(P.e[e].tile_start);
   const int per = int(P.e[e].tiles_per);
   Loc L;
@@ -679,42 +669,43 @@ __global__ __launch_bounds__(Tile<T>::NT) void k_gram_fast(const Phase P) {
   }
 
   if (P.flags & kRowSum) {
-    // part[Jb][i] = sum over column block Jb of |A0_ij|, from the fp32 accumulators
+    // part[b][i] = sum over the 64 columns of block b of |A0_ij|, from the fp32
+    // accumulators.  The reduction tree is fixed for every tile size: each
+    // 32 x 32 MFMA block is reduced first (rows: across its 32 lanes; columns:
+    // over its 16 registers, then the lane pair), then two adjacent 32-blocks
+    // are added.  Off-diagonal tiles also emit the partials of the mirrored
+    // tile (column sums), so every row of A0 gets kp / 64 partials.
     __syncthreads();
     float* part = reinterpret_cast<float*>(w + WL.part);
-    constexpr int NWN = Tile<T>::NW / 2;
-    float* rs = reinterpret_cast<float*>(smem);       // [NW/2][T] row sums per wn
-    float* cs = rs + NWN * T;                         // [2][T] column sums per wm
+    constexpr int NB = T / 32;
+    float* rs = reinterpret_cast<float*>(smem);       // [NB][T] row sums over 32-column blocks
+    float* cs = rs + NB * T;                          // [NB][T] column sums over 32-row blocks
     const int lane = threadIdx.x & 63;
     const int wm = wave_m(Tile<T>::NW), wn = wave_n(Tile<T>::NW);
 #pragma unroll
     for (int fm = 0; fm < FM; ++fm)
 #pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        float x = 0.f;
+      for (int fn = 0; fn < FN; ++fn) {
 #pragma unroll
-        for (int fn = 0; fn < FN; ++fn) x += fabsf(acc[fm][fn][v]);
+        for (int v = 0; v < 16; ++v) {
+          float x = fabsf(acc[fm][fn][v]);
 #pragma unroll
-        for (int off = 16; off >= 1; off >>= 1) x += __shfl_xor(x, off, 64);
-        if ((lane & 31) == 0) rs[wn * T + acc_row<T>(wm, fm, v)] = x;
+          for (int off = 16; off >= 1; off >>= 1) x += __shfl_xor(x, off, 64);
+          if ((lane & 31) == 0) rs[((wn * Tile<T>::TWN) / 32 + fn) * T + acc_row<T>(wm, fm, v)] = x;
+        }
+        float y = 0.f;
+#pragma unroll
+        for (int v = 0; v < 16; ++v) y += fabsf(acc[fm][fn][v]);
+        y += __shfl_xor(y, 32, 64);
+        if (lane < 32) cs[((wm * Tile<T>::TWM) / 32 + fm) * T + acc_col<T>(wn, fn)] = y;
       }
-#pragma unroll
-    for (int fn = 0; fn < FN; ++fn) {
-      float x = 0.f;
-#pragma unroll
-      for (int fm = 0; fm < FM; ++fm)
-#pragma unroll
-        for (int v = 0; v < 16; ++v) x += fabsf(acc[fm][fn][v]);
-      x += __shfl_xor(x, 32, 64);
-      if (lane < 32) cs[wm * T + acc_col<T>(wn, fn)] = x;
-    }
     __syncthreads();
-    for (int r = threadIdx.x; r < T; r += Tile<T>::NT) {
-      float x = 0.f;
-#pragma unroll
-      for (int q = 0; q < NWN; ++q) x += rs[q * T + r];
-      part[int64_t(J) * kp + I * T + r] = x;
-      if (I != J) part[int64_t(I) * kp + J * T + r] = cs[r] + cs[T + r];
+    constexpr int NB64 = T / 64;
+    for (int q = threadIdx.x; q < NB64 * T; q += Tile<T>::NT) {
+      const int b = q / T, r = q - b * T;
+      part[int64_t(J * NB64 + b) * kp + I * T + r] = rs[(2 * b) * T + r] + rs[(2 * b + 1) * T + r];
+      if (I != J)
+        part[int64_t(I * NB64 + b) * kp + J * T + r] = cs[(2 * b) * T + r] + cs[(2 * b + 1) * T + r];
     }
   }
 }

@@ -74,8 +74,9 @@ constexpr int kNumCfg = 3;
 TM_HD int cfg_tile(int cfg) { return cfg == 0 ? 256 : (cfg == 1 ? 128 : 64); }
 
 // Logical blocks per matrix of each kernel.
+// The numbering matches the TM_PHASE_* timing phases of turbomuon.h.
 enum Kind { kKindTransposeIn, kKindFrob, kKindGram, kKindAolVector, kKindPoly,
-            kKindUpdate, kKindApplyScale, kKindCopyOut, kKindLoadIn, kKindScaleA };
+            kKindUpdate, kKindApplyScale, kKindCopyOut, kKindLoadIn, kKindScaleA, kNumKinds };
 constexpr int kTransposeTile = 64;
 constexpr int kElemBlock = 2048;     // elements per block of the elementwise kernels
 

@@ -77,8 +77,14 @@ struct Loc {
 };
 
 __device__ inline Loc locate(const Phase& P, int lid) {
-  int e = 0;
-  while (e + 1 < P.nent && lid >= int(P.e[e + 1].tile_start)) ++e;
+  // last entry whose first block is <= lid (entries without blocks share the
+  // start of the next entry and are never the last such entry)
+  int e = 0, hi = P.nent - 1;
+  while (e < hi) {
+    const int mid = (e + hi + 1) >> 1;
+    if (lid >= int(P.e[mid].tile_start)) e = mid;
+    else hi = mid - 1;
+  }
   const int r = lid - int(P.e[e].tile_start);
   const int per = int(P.e[e].tiles_per);
   Loc L;
