@@ -37,7 +37,7 @@ import numpy as np
 
 CONSTANT_TRIPLE = (3.4445, -4.7750, 2.0315)
 
-PRECONDS = ("none", "frobenius", "aol")
+PRECONDS = ("none", "frobenius", "aol", "schatten4")
 
 
 def _coeff_list(t: int, coeffs) -> list:
@@ -78,6 +78,17 @@ def frobenius_scale(X0: np.ndarray) -> np.ndarray:
     return X0 * (1.0 / f)
 
 
+def schatten4_scale(A0: np.ndarray) -> float:
+    """1 / ||X0||_S4 from the first Gram (appendix on other pre-conditionings).
+
+    ||X||_S4 = (sum_i sigma_i^4)^(1/4), and the eigenvalues of A0 = X0^T X0 are
+    the sigma_i^2, so ||X||_S4 = ||A0||_F^(1/2): the scale comes from the
+    Frobenius norm of the Gram Algorithm 2 forms anyway.  A zero Gram maps to 0.
+    """
+    f = np.linalg.norm(A0)
+    return 0.0 if f == 0 else 1.0 / np.sqrt(f)
+
+
 def newton_schulz_alg2(X0: np.ndarray, t: int, coeffs=None,
                        precond: str = "aol") -> np.ndarray:
     """Algorithms 1 and 2 literally: Gram X^T X, column scaling, X <- aX + XB.
@@ -85,7 +96,10 @@ def newton_schulz_alg2(X0: np.ndarray, t: int, coeffs=None,
     precond="aol" is Algorithm 2 (Turbo-Muon): the Gram A0 of the raw input
     gives the AOL vector s, X1 = X0 diag(s) and A1 = diag(s) A0 diag(s) without
     a second product.  precond="frobenius" is Algorithm 1 (Muon): X1 =
-    X0 / ||X0||_F and A1 = X1^T X1.  precond="none" starts from X1 = X0.
+    X0 / ||X0||_F and A1 = X1^T X1.  precond="schatten4" (appendix on other
+    pre-conditionings) takes the scale 1 / ||X0||_S4 = ||A0||_F^(-1/2) from the
+    first Gram, X1 = X0 / ||X0||_S4 and A1 = A0 / ||X0||_S4^2, again without a
+    second product.  precond="none" starts from X1 = X0.
     Then for k = 1..t: A_k = X_k^T X_k (k >= 2), B_k = b_k A_k + c_k A_k A_k,
     X_{k+1} = a_k X_k + X_k B_k.  t = 0 returns X1.
     """
@@ -103,6 +117,11 @@ def newton_schulz_alg2(X0: np.ndarray, t: int, coeffs=None,
     elif precond == "frobenius":
         X = frobenius_scale(X0)              # s = 1/||X0||_F ; X1 = X0 s
         A = X.T @ X                          # A1 = X1^T X1
+    elif precond == "schatten4":
+        A0 = X0.T @ X0                       # initial matmul
+        g = schatten4_scale(A0)              # 1 / ||X0||_S4
+        X = X0 * g                           # X1 = X0 / ||X0||_S4
+        A = A0 * (g * g)                     # A1 = A0 / ||X0||_S4^2
     else:
         X = X0.copy()
         A = X.T @ X

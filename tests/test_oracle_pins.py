@@ -47,7 +47,7 @@ def rand_orth(rng, n):
 # P1: the loop equals U phi(Sigma) V^T (textbook SVD + scalar polynomial)
 # --------------------------------------------------------------------------
 @pytest.mark.parametrize("m,n", [(17, 33), (40, 40), (64, 20), (1, 7), (7, 1), (96, 96)])
-@pytest.mark.parametrize("precond", ["aol", "frobenius", "none"])
+@pytest.mark.parametrize("precond", ["aol", "frobenius", "schatten4", "none"])
 def test_p1_loop_matches_spectral_closed_form(m, n, precond):
     rng = np.random.default_rng(m * 1000 + n)
     X = synth.power_law_matrix(m, n, 0.8, seed=m + n)
@@ -143,7 +143,7 @@ def test_scaled_orthogonal_rows_and_columns_are_restored():
 
 def test_zero_matrix_and_zero_rows():
     Z = np.zeros((4, 6))
-    for pre in ("aol", "frobenius", "none"):
+    for pre in ("aol", "frobenius", "schatten4", "none"):
         assert np.all(O.orthogonalize(Z, 4, None, pre) == 0)
     X = synth.power_law_matrix(5, 8, 1.0, seed=1)
     X[2] = 0.0
@@ -295,3 +295,54 @@ def test_p5_table1_muon_baseline_polar_error():
     Z = O.orthogonalize(X, gold["iters"], None, gold["precond"])
     e = O.eps_polar(Z, X)
     assert abs(e - gold["polar_error"]) <= gold["tolerance"]
+
+
+# --------------------------------------------------------------------------
+# Schatten-4 pre-conditioning (appendix on other pre-conditioning strategies)
+# --------------------------------------------------------------------------
+@pytest.mark.parametrize("m,n", [(20, 35), (35, 20), (24, 24), (1, 9)])
+def test_schatten4_scale_is_the_svd_norm(m, n):
+    """X1 = X / (sum sigma^4)^(1/4): the Gram route equals LAPACK's singular values."""
+    X = synth.power_law_matrix(m, n, 0.8, seed=m + n)
+    sv = np.linalg.svd(X, compute_uv=False)
+    s4 = np.sum(sv ** 4) ** 0.25
+    assert relF(O.preconditioned(X, "schatten4"), X / s4) <= 1e-13
+    assert relF(O.preconditioned(X, "schatten4", side="cols"), X / s4) <= 1e-13
+
+
+def test_schatten4_bounds_and_rank_one():
+    """sigma_max <= ||X||_S4 <= ||X||_F; equality for rank one, where X1 = u v^T."""
+    for seed in range(3):
+        X = synth.power_law_matrix(40, 70, 0.5, seed)
+        X1 = O.preconditioned(X, "schatten4")
+        assert np.linalg.norm(X1, 2) <= 1 + 1e-14
+        assert np.linalg.norm(X1) >= 1 - 1e-14            # ||X||_F >= ||X||_S4
+    rng = np.random.default_rng(3)
+    u, v = rng.standard_normal(7), rng.standard_normal(11)
+    X = 2.5 * np.outer(u, v)
+    uv = np.outer(u / np.linalg.norm(u), v / np.linalg.norm(v))
+    assert np.max(np.abs(O.preconditioned(X, "schatten4") - uv)) <= 1e-14
+    assert np.max(np.abs(O.orthogonalize(X, 4, None, "schatten4") - phi(1.0, [TRIPLE] * 4) * uv)) <= 1e-13
+
+
+@pytest.mark.parametrize("m,n", [(20, 35), (24, 24)])
+def test_schatten4_invariances(m, n):
+    """A spectral scale: orthogonal equivariance O(U X V) = U O(X) V and O(aX) = sign(a) O(X)."""
+    rng = np.random.default_rng(m + 7 * n)
+    X = synth.power_law_matrix(m, n, 0.8, seed=5)
+    Z = O.orthogonalize(X, 4, None, "schatten4")
+    U, V = rand_orth(rng, m), rand_orth(rng, n)
+    assert relF(O.orthogonalize(U @ X @ V, 4, None, "schatten4"), U @ Z @ V) <= 1e-11
+    assert relF(O.orthogonalize(-0.3 * X, 4, None, "schatten4"), -Z) <= 1e-12
+
+
+@pytest.mark.parametrize("n", [64, 256, 512])
+def test_schatten4_initial_polar_error_ordering(n):
+    """The appendix figure of initialisations: Schatten-4 improves on Frobenius and AOL
+    is better still (N(0,1) inputs).  Schatten-4 below Frobenius is also a theorem:
+    every sigma_i / ||X||_S4 lies between sigma_i / ||X||_F and 1."""
+    for seed in range(2):
+        X = synth.gaussian_matrix(n, n, seed)
+        Q = O.polar_factor(X)
+        e = {p: O.eps_polar(O.preconditioned(X, p), X, Q) for p in ("frobenius", "schatten4", "aol")}
+        assert e["aol"] < e["schatten4"] < e["frobenius"]
