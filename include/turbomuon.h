@@ -9,7 +9,9 @@
  *   X1 = X0 scaled by s, A1 = diag(s) A0 diag(s) (no second product), then for
  *   k = 1..t:  A_k = Gram(X_k) (k >= 2), B_k = b_k A_k + c_k A_k^2,
  *              X_{k+1} = a_k X_k + X_k B_k                (Algorithm 1, eq. (ns_quintic))
- *   Algorithm 1 (Muon) instead scales by 1 / ||X0||_F (precond FROBENIUS).
+ *   Algorithm 1 (Muon) instead scales by 1 / ||X0||_F (precond FROBENIUS); the
+ *   Schatten-4 variant of the paper's appendix on other pre-conditionings scales
+ *   by (sum_i sigma_i^4)^(-1/4) = ||A0||_F^(-1/2), again from the first Gram.
  *
  * Orientation.  For an m x n input with m <= n (square included) the Gram is
  * the m x m matrix X X^T and the AOL vector scales rows; for m > n it is the
@@ -57,6 +59,8 @@ typedef int tm_status;
 #define TM_PRECOND_NONE       0  /* X1 = X0 */
 #define TM_PRECOND_FROBENIUS  1  /* X1 = X0 / ||X0||_F: Algorithm 1 (Muon); zero stays zero */
 #define TM_PRECOND_AOL        2  /* X1 = AOL(X0), eq. (aol): Algorithm 2 (Turbo-Muon) */
+#define TM_PRECOND_SCHATTEN4  3  /* X1 = X0 / ||X0||_S4 with ||X0||_S4 = ||A0||_F^(1/2) from the
+                                    first Gram (appendix on other pre-conditionings) */
 
 /* Limits checked by every entry point. */
 #define TM_MAX_DIM    65536      /* m, n <= TM_MAX_DIM */
@@ -121,7 +125,7 @@ tm_status tm_release_workspaces(void);
 
 /* Kernel phases, as counted by the timing hooks below. */
 #define TM_PHASE_TRANSPOSE_IN  0  /* tall input: W = X^T */
-#define TM_PHASE_FROB          1  /* partial sums of squares (Algorithm 1, first line) */
+#define TM_PHASE_FROB          1  /* partial sums of squares of X0 (Algorithm 1, first line) or of A0 (Schatten-4) */
 #define TM_PHASE_GRAM          2  /* A = X X^T, upper tiles (+ AOL row sums at iteration 1) */
 #define TM_PHASE_AOL_VECTOR    3  /* s_i = 1/sqrt(row sum) (Algorithm 2, second line) */
 #define TM_PHASE_POLY          4  /* B = b A + c A^2 */

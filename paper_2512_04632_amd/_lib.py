@@ -21,7 +21,7 @@ TM_ERR_UNSUPPORTED = -2
 TM_ERR_NO_MEMORY = -3
 TM_ERR_HIP = -4
 
-PRECOND = {"none": 0, "frobenius": 1, "frob": 1, "aol": 2}
+PRECOND = {"none": 0, "frobenius": 1, "frob": 1, "aol": 2, "schatten4": 3, "s4": 3}
 PHASES = {"transpose_in": 0, "frob": 1, "gram": 2, "aol_vector": 3, "poly": 4, "update": 5,
           "apply_scale": 6, "copy_out": 7, "load_in": 8, "scale_a": 9}
 TM_MAX_DIM = 65536
@@ -123,7 +123,7 @@ def orthogonalize(x, iters: int = 4, coeffs: Optional[Sequence] = None, precond=
     """Orthogonalize x in place: (m, n) or (batch, m, n), contiguous, bf16 or fp32, on a GPU.
 
     iters Newton-Schulz iterations after the pre-conditioning ("aol",
-    "frobenius" or "none"); coeffs is an optional list of (a, b, c) per
+    "frobenius", "schatten4" or "none"); coeffs is an optional list of (a, b, c) per
     iteration.  Work is enqueued on `stream` (default: the current stream).
     Returns x.
     """

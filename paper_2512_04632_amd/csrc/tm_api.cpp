@@ -246,26 +246,50 @@ tm_status launch(const Plan& pl, int kind, int cfg, int src, int dst, float a, f
 }
 
 // bf16: zero-padded tiled workspace, matrix-core kernels of tm_fast.hip.
+// Scale vector s from the first Gram (its flags carry the row partials):
+// AOL (Algorithm 2, second line) s_i = 1 / sqrt(row sum of |A0|); Schatten-4
+// the uniform ||A0||_F^(-1/2), summed from the squares' row partials.  `part`
+// is the column granularity of the row partials.
+tm_status gram_scale(const Plan& pl, int precond, int part) {
+  if (precond == TM_PRECOND_AOL)
+    return launch(pl, tmk::kKindAolVector, 0, 0, 0, 0.f, 0.f, 0.f, 0u, part, false);
+  tm_status s = launch(pl, tmk::kKindFrob, 0, 0, 0, 0.f, 0.f, 0.f, tmk::kFromPart, part, false);
+  if (s == TM_OK)
+    s = launch(pl, tmk::kKindAolVector, 0, 0, 0, 0.f, 0.f, 0.f, tmk::kFrob | tmk::kS4, 0, false);
+  return s;
+}
+
+// Row-partial flags of the first Gram for a pre-conditioning.
+uint32_t first_gram_flags(int precond) {
+  if (precond == TM_PRECOND_AOL) return tmk::kRowSum;
+  if (precond == TM_PRECOND_SCHATTEN4) return tmk::kRowSum | tmk::kRowSq;
+  return 0u;
+}
+
+// bf16: zero-padded tiled workspace, matrix-core kernels of tm_fast.hip.
 tm_status plan_bf16(const Plan& pl, int iters, const float* coeffs, int precond, int tcfg) {
-  const bool aol = precond == TM_PRECOND_AOL, frob = precond == TM_PRECOND_FROBENIUS;
+  const bool frob = precond == TM_PRECOND_FROBENIUS;
+  const bool from_gram = precond == TM_PRECOND_AOL || precond == TM_PRECOND_SCHATTEN4;
+  const bool scaled = from_gram || frob;
+  const uint32_t rflags = first_gram_flags(precond);
   const int gcfg = choose_sym_cfg(tmk::kKindGram, tcfg, *pl.items);
   const int pcfg = choose_sym_cfg(tmk::kKindPoly, tcfg, *pl.items);
-  const int T = tmk::kMinTile;   // the matrix-core Gram emits row sums per 64 columns
+  const int part = tmk::kMinTile;   // the matrix-core Gram emits row partials per 64 columns
   tm_status s = TM_OK;
-  if (iters > 0 || aol) s = launch(pl, tmk::kKindLoadIn, 0, 0, 0, 0.f, 0.f, 0.f, 0u, 0, false);
+  if (iters > 0 || from_gram) s = launch(pl, tmk::kKindLoadIn, 0, 0, 0, 0.f, 0.f, 0.f, 0u, 0, false);
   if (s == TM_OK && frob) {  // Algorithm 1, first line: s = 1 / ||X0||_F
     s = launch(pl, tmk::kKindFrob, 0, 0, 0, 0.f, 0.f, 0.f, 0u, 0, false);
     if (s == TM_OK) s = launch(pl, tmk::kKindAolVector, 0, 0, 0, 0.f, 0.f, 0.f, tmk::kFrob, 0, false);
   }
   if (s != TM_OK) return s;
   if (iters == 0) {
-    if (aol) {
-      s = launch(pl, tmk::kKindGram, gcfg, tmk::kSlotFirst, 0, 0.f, 0.f, 0.f,
-                 tmk::kRowSum | tmk::kA32, 0, false);
-      if (s == TM_OK) s = launch(pl, tmk::kKindAolVector, 0, 0, 0, 0.f, 0.f, 0.f, 0u, T, false);
+    if (from_gram) {
+      s = launch(pl, tmk::kKindGram, gcfg, tmk::kSlotFirst, 0, 0.f, 0.f, 0.f, rflags | tmk::kA32, 0,
+                 false);
+      if (s == TM_OK) s = gram_scale(pl, precond, part);
       if (s != TM_OK) return s;
     }
-    if (aol || frob) s = launch(pl, tmk::kKindApplyScale, 0, 0, 0, 0.f, 0.f, 0.f, 0u, 0, false);
+    if (scaled) s = launch(pl, tmk::kKindApplyScale, 0, 0, 0, 0.f, 0.f, 0.f, 0u, 0, false);
     return s;
   }
   int src = tmk::kSlotFirst;
@@ -275,11 +299,10 @@ tm_status plan_bf16(const Plan& pl, int iters, const float* coeffs, int precond,
     const float c = coeffs ? coeffs[3 * (it - 1) + 2] : kC;
     const int dst = it == iters ? tmk::kSlotFinal : (it % 2 == 1 ? tmk::kSlotAlt1 : tmk::kSlotAlt2);
     const bool first = it == 1;
-    const uint32_t scale = (first && (aol || frob)) ? tmk::kScale : 0u;
-    const uint32_t gflags = ((first && aol) ? tmk::kRowSum : 0u) | (scale ? tmk::kA32 : 0u);
+    const uint32_t scale = (first && scaled) ? tmk::kScale : 0u;
+    const uint32_t gflags = (first ? rflags : 0u) | (scale ? tmk::kA32 : 0u);
     s = launch(pl, tmk::kKindGram, gcfg, src, 0, 0.f, 0.f, 0.f, gflags, 0, false);
-    if (s == TM_OK && first && aol)  // Algorithm 2, second line: the AOL vector
-      s = launch(pl, tmk::kKindAolVector, 0, 0, 0, 0.f, 0.f, 0.f, 0u, T, false);
+    if (s == TM_OK && first && from_gram) s = gram_scale(pl, precond, part);
     if (s == TM_OK && scale)         // A1 = diag(s) A0 diag(s), one rounding
       s = launch(pl, tmk::kKindScaleA, 0, 0, 0, 0.f, 0.f, 0.f, 0u, 0, false);
     if (s == TM_OK) s = launch(pl, tmk::kKindPoly, pcfg, 0, 0, a, b, c, scale, 0, false);
@@ -293,16 +316,20 @@ tm_status plan_bf16(const Plan& pl, int iters, const float* coeffs, int precond,
 tm_status plan_f32(const Plan& pl, int iters, const float* coeffs, int precond) {
   const std::vector<Item>& items = *pl.items;
   tm_status s = TM_OK;
+  const bool frob = precond == TM_PRECOND_FROBENIUS;
+  const bool from_gram = precond == TM_PRECOND_AOL || precond == TM_PRECOND_SCHATTEN4;
+  const bool scaled = from_gram || frob;
+  const uint32_t rflags = first_gram_flags(precond);
   bool any_tall = false;
   for (const Item& it : items) any_tall = any_tall || it.tall;
-  if (any_tall && (iters > 0 || precond == TM_PRECOND_AOL)) {
+  if (any_tall && (iters > 0 || from_gram)) {
     s = launch(pl, tmk::kKindTransposeIn, 0, 0, 0, 0.f, 0.f, 0.f, 0u, 0, true);
     if (s != TM_OK) return s;
   }
   const int gcfg = choose_cfg(tmk::kKindGram, items);
   const int pcfg = choose_cfg(tmk::kKindPoly, items);
   const int ucfg = choose_cfg(tmk::kKindUpdate, items);
-  const bool aol = precond == TM_PRECOND_AOL, frob = precond == TM_PRECOND_FROBENIUS;
+  const int part = tmk::cfg_tile(gcfg);   // row partials per Gram tile column block
 
   if (frob) {  // Algorithm 1, first line: s = 1 / ||X0||_F
     s = launch(pl, tmk::kKindFrob, 0, 0, 0, 0.f, 0.f, 0.f, 0u, 0, false);
@@ -310,14 +337,13 @@ tm_status plan_f32(const Plan& pl, int iters, const float* coeffs, int precond) 
     if (s != TM_OK) return s;
   }
   if (iters == 0) {
-    if (aol) {
-      s = launch(pl, tmk::kKindGram, gcfg, tmk::kSlotFirst, 0, 0.f, 0.f, 0.f,
-                 tmk::kRowSum | tmk::kA32, 0, false);
-      if (s == TM_OK)
-        s = launch(pl, tmk::kKindAolVector, 0, 0, 0, 0.f, 0.f, 0.f, 0u, tmk::cfg_tile(gcfg), false);
+    if (from_gram) {
+      s = launch(pl, tmk::kKindGram, gcfg, tmk::kSlotFirst, 0, 0.f, 0.f, 0.f, rflags | tmk::kA32, 0,
+                 false);
+      if (s == TM_OK) s = gram_scale(pl, precond, part);
       if (s != TM_OK) return s;
     }
-    if (aol || frob) s = launch(pl, tmk::kKindApplyScale, 0, 0, 0, 0.f, 0.f, 0.f, 0u, 0, false);
+    if (scaled) s = launch(pl, tmk::kKindApplyScale, 0, 0, 0, 0.f, 0.f, 0.f, 0u, 0, false);
     return s;
   }
 
@@ -331,11 +357,10 @@ tm_status plan_f32(const Plan& pl, int iters, const float* coeffs, int precond) 
     const int dst = (it == iters && iters > 1) ? tmk::kSlotFinal
                                                : (it % 2 == 1 ? tmk::kSlotAlt1 : tmk::kSlotAlt2);
     const bool first = it == 1;
-    const uint32_t scale = (first && (aol || frob)) ? tmk::kScale : 0u;
-    const uint32_t gflags = ((first && aol) ? tmk::kRowSum : 0u) | (scale ? tmk::kA32 : 0u);
+    const uint32_t scale = (first && scaled) ? tmk::kScale : 0u;
+    const uint32_t gflags = (first ? rflags : 0u) | (scale ? tmk::kA32 : 0u);
     s = launch(pl, tmk::kKindGram, gcfg, src, 0, 0.f, 0.f, 0.f, gflags, 0, false);
-    if (s == TM_OK && first && aol)  // Algorithm 2, second line: the AOL vector
-      s = launch(pl, tmk::kKindAolVector, 0, 0, 0, 0.f, 0.f, 0.f, 0u, tmk::cfg_tile(gcfg), false);
+    if (s == TM_OK && first && from_gram) s = gram_scale(pl, precond, part);
     if (s == TM_OK) s = launch(pl, tmk::kKindPoly, pcfg, 0, 0, a, b, c, scale, 0, false);
     if (s == TM_OK) s = launch(pl, tmk::kKindUpdate, ucfg, src, dst, a, b, c, scale, 0, false);
     if (s != TM_OK) return s;
@@ -376,7 +401,8 @@ tm_status run(std::vector<Item>& items, int esz, int iters, const float* coeffs,
 tm_status check_common(int iters, const float* coeffs, int precond) {
   if (iters < 0 || iters > TM_MAX_ITERS)
     return fail(TM_ERR_INVALID_ARG, "iters out of range [0, " + std::to_string(TM_MAX_ITERS) + "]");
-  if (precond != TM_PRECOND_NONE && precond != TM_PRECOND_FROBENIUS && precond != TM_PRECOND_AOL)
+  if (precond != TM_PRECOND_NONE && precond != TM_PRECOND_FROBENIUS && precond != TM_PRECOND_AOL &&
+      precond != TM_PRECOND_SCHATTEN4)
     return fail(TM_ERR_INVALID_ARG, "unknown precond " + std::to_string(precond));
   (void)coeffs;
   return TM_OK;

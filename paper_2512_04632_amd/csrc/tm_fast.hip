@@ -669,7 +669,8 @@ __global__ __launch_bounds__(Tile<T>::NT) void k_gram_fast(const Phase P) {
   }
 
   if (P.flags & kRowSum) {
-    // part[b][i] = sum over the 64 columns of block b of |A0_ij|, from the fp32
+    // part[b][i] = sum over the 64 columns of block b of |A0_ij| (with kRowSq:
+    // A0_ij^2, whose total is ||A0||_F^2 for the Schatten-4 scale), from the fp32
     // accumulators.  The reduction tree is fixed for every tile size: each
     // 32 x 32 MFMA block is reduced first (rows: across its 32 lanes; columns:
     // over its 16 registers, then the lane pair), then two adjacent 32-blocks
@@ -677,6 +678,8 @@ __global__ __launch_bounds__(Tile<T>::NT) void k_gram_fast(const Phase P) {
     // tile (column sums), so every row of A0 gets kp / 64 partials.
     __syncthreads();
     float* part = reinterpret_cast<float*>(w + WL.part);
+    const bool sq = (P.flags & kRowSq) != 0u;   // Schatten-4: sums of A0_ij^2
+    auto mag = [sq](float x) { return sq ? x * x : fabsf(x); };
     constexpr int NB = T / 32;
     float* rs = reinterpret_cast<float*>(smem);       // [NB][T] row sums over 32-column blocks
     float* cs = rs + NB * T;                          // [NB][T] column sums over 32-row blocks
@@ -688,14 +691,14 @@ __global__ __launch_bounds__(Tile<T>::NT) void k_gram_fast(const Phase P) {
       for (int fn = 0; fn < FN; ++fn) {
 #pragma unroll
         for (int v = 0; v < 16; ++v) {
-          float x = fabsf(acc[fm][fn][v]);
+          float x = mag(acc[fm][fn][v]);
 #pragma unroll
           for (int off = 16; off >= 1; off >>= 1) x += __shfl_xor(x, off, 64);
           if ((lane & 31) == 0) rs[((wn * Tile<T>::TWN) / 32 + fn) * T + acc_row<T>(wm, fm, v)] = x;
         }
         float y = 0.f;
 #pragma unroll
-        for (int v = 0; v < 16; ++v) y += fabsf(acc[fm][fn][v]);
+        for (int v = 0; v < 16; ++v) y += mag(acc[fm][fn][v]);
         y += __shfl_xor(y, 32, 64);
         if (lane < 32) cs[((wm * Tile<T>::TWM) / 32 + fm) * T + acc_col<T>(wn, fn)] = y;
       }

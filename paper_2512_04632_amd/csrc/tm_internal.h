@@ -40,6 +40,9 @@ constexpr uint32_t kScale = 1u;   // first iteration after AOL / Frobenius: appl
 constexpr uint32_t kRowSum = 2u;  // Gram epilogue emits AOL row-sum partials
 constexpr uint32_t kFrob = 4u;    // AOL-vector kernel: uniform s from the Frobenius partials
 constexpr uint32_t kA32 = 8u;     // Gram stores A0 in fp32 (first iteration, before scaling)
+constexpr uint32_t kRowSq = 16u;  // with kRowSum: partials of A0_ij^2 instead of |A0_ij|
+constexpr uint32_t kS4 = 32u;     // with kFrob: s = (sum of the partials)^(-1/4) (Schatten-4)
+constexpr uint32_t kFromPart = 64u;  // Frobenius-partial kernel sums the Gram's row partials
 
 // Entry flags.
 constexpr uint32_t kTall = 1u;    // the user matrix is N x k (m > n); work on its transpose

@@ -405,7 +405,8 @@ __device__ inline void store_sym(const f32x16_t (&acc)[C::FM][C::FN], T* __restr
 
 // ---------------------------------------------------------------- kernels
 // A = Y Y^T (upper tiles).  With kRowSum: part[Jb][i] = sum_{j in block Jb} |A_ij|
-// for every row i and column block Jb, each written exactly once.
+// (A_ij^2 with kRowSq) for every row i < k and column block Jb, each written
+// exactly once.
 template <typename T, class C>
 __global__ __launch_bounds__(256) void k_gram(const Phase P) {
   __shared__ __attribute__((aligned(16))) char smem[C::LDS];
@@ -431,6 +432,8 @@ __global__ __launch_bounds__(256) void k_gram(const Phase P) {
 
   if (P.flags & kRowSum) {
     float* part = reinterpret_cast<float*>(w + WL.part);
+    const bool sq = (P.flags & kRowSq) != 0u;   // Schatten-4: sums of A0_ij^2
+    auto mag = [sq](float x) { return sq ? x * x : fabsf(x); };
     float* rs = reinterpret_cast<float*>(smem);            // [2][BM] row sums per wn
     float* cs = rs + 2 * C::BM;                            // [2][BN] column sums per wm
     const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
@@ -442,7 +445,7 @@ __global__ __launch_bounds__(256) void k_gram(const Phase P) {
       for (int v = 0; v < 16; ++v) {
         float x = 0.f;
 #pragma unroll
-        for (int fn = 0; fn < C::FN; ++fn) x += fabsf(acc[fm][fn][v]);
+        for (int fn = 0; fn < C::FN; ++fn) x += mag(acc[fm][fn][v]);
 #pragma unroll
         for (int off = 16; off >= 1; off >>= 1) x += __shfl_xor(x, off, 64);
         if ((lane & 31) == 0) rs[wn * C::BM + acc_row<C>(wm, fm, v)] = x;
@@ -453,7 +456,7 @@ __global__ __launch_bounds__(256) void k_gram(const Phase P) {
 #pragma unroll
       for (int fm = 0; fm < C::FM; ++fm)
 #pragma unroll
-        for (int v = 0; v < 16; ++v) x += fabsf(acc[fm][fn][v]);
+        for (int v = 0; v < 16; ++v) x += mag(acc[fm][fn][v]);
       x += __shfl_xor(x, 32, 64);
       if (lane < 32) cs[wm * C::BN + acc_col<C>(wn, fn)] = x;
     }
@@ -596,19 +599,32 @@ __device__ inline float block_sum_256(float x, float* red) {
 }
 
 // Partial sums of squares of each user matrix (any orientation: ||X||_F = ||X^T||_F).
+// With kFromPart: partial sums of the first Gram's row partials part[b][i]
+// (i < k, P.aux columns per block b), i.e. of ||A0||_F^2 for Schatten-4.
 template <typename T>
 __global__ __launch_bounds__(256) void k_frob_partial(const Phase P) {
   __shared__ float red[4];
   const Loc L = locate(P, blockIdx.x);
   const Entry& E = P.e[L.ent];
-  const int64_t total = int64_t(E.k) * E.N;
+  const bool from_part = (P.flags & kFromPart) != 0u;
+  const int64_t nb = int64_t(cdiv(E.kp, uint32_t(max(P.aux, 1))));
+  const int64_t total = from_part ? nb * E.k : int64_t(E.k) * E.N;
   const int64_t chunk = (total + kFrobBlocks - 1) / kFrobBlocks;
   const int64_t lo = chunk * L.tile, hi = min(total, lo + chunk);
   const T* X = user_of<T>(E, L.mat);
+  const float* part = reinterpret_cast<const float*>(ws_of<T>(P, E, L.mat) +
+                                                     ws_layout(E.kp, E.Np, sizeof(T)).part);
   float x = 0.f;
-  for (int64_t i = lo + threadIdx.x; i < hi; i += 256) {
-    const float v = Elem<T>::to_f(X[i]);
-    x += v * v;
+  if (from_part) {
+    for (int64_t q = lo + threadIdx.x; q < hi; q += 256) {
+      const int64_t b = q / E.k, i = q - b * E.k;
+      x += part[b * E.kp + i];
+    }
+  } else {
+    for (int64_t i = lo + threadIdx.x; i < hi; i += 256) {
+      const float v = Elem<T>::to_f(X[i]);
+      x += v * v;
+    }
   }
   x = block_sum_256(x, red);
   if (threadIdx.x == 0) {
@@ -618,7 +634,8 @@ __global__ __launch_bounds__(256) void k_frob_partial(const Phase P) {
 }
 
 // s_i = 1/sqrt(sum_Jb part[Jb][i]) (0 for a zero sum), or with kFrob the
-// uniform 1/sqrt(sum of the Frobenius partials).  Fixed summation order.
+// uniform 1/sqrt(sum of the Frobenius partials), with kFrob | kS4 the uniform
+// (sum of the partials)^(-1/4).  Fixed summation order.
 template <typename T>
 __global__ __launch_bounds__(256) void k_aol_vector(const Phase P) {
   const Loc L = locate(P, blockIdx.x);
@@ -640,7 +657,8 @@ __global__ __launch_bounds__(256) void k_aol_vector(const Phase P) {
       for (int b = 0; b < nb; ++b) r += part[int64_t(b) * kp + i];
     }
   }
-  s[i] = r >= 1.17549435e-38f ? 1.0f / sqrtf(r) : 0.f;   // padding rows: 0
+  const float q = (P.flags & kS4) ? sqrtf(r) : r;         // Schatten-4: ||A0||_F
+  s[i] = r >= 1.17549435e-38f ? 1.0f / sqrtf(q) : 0.f;   // padding rows: 0
 }
 
 // X1 = diag(s) X0 in place on the user matrix (rows of the wide view).

@@ -39,6 +39,9 @@ def test_constants_match_header():
     assert d["TM_PRECOND_NONE"] == tm.PRECOND["none"]
     assert d["TM_PRECOND_FROBENIUS"] == tm.PRECOND["frobenius"]
     assert d["TM_PRECOND_AOL"] == tm.PRECOND["aol"]
+    assert d["TM_PRECOND_SCHATTEN4"] == tm.PRECOND["schatten4"]
+    phases = {k[len("TM_PHASE_"):].lower(): v for k, v in d.items() if k.startswith("TM_PHASE_")}
+    assert phases == tm.PHASES and d["TM_NUM_PHASES"] == len(tm.PHASES)
     assert d["TM_MAX_DIM"] == tm.TM_MAX_DIM and d["TM_MAX_ITERS"] == tm.TM_MAX_ITERS
 
 
@@ -62,7 +65,7 @@ FAKE = ctypes.c_void_p(0x1000)   # never dereferenced: validation fails or batch
     (4, 4, -1, 4, 2, tm.TM_ERR_INVALID_ARG),
     (4, 4, 1, -1, 2, tm.TM_ERR_INVALID_ARG),
     (4, 4, 1, 65, 2, tm.TM_ERR_INVALID_ARG),
-    (4, 4, 1, 4, 3, tm.TM_ERR_INVALID_ARG),
+    (4, 4, 1, 4, 4, tm.TM_ERR_INVALID_ARG),
     (4, 4, 1, 4, -1, tm.TM_ERR_INVALID_ARG),
     (4, 4, 0, 4, 2, tm.TM_OK),                 # empty batch: no-op
 ])

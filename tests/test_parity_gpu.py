@@ -53,7 +53,8 @@ SHAPES = [(1, 1), (1, 8), (8, 1), (5, 3), (17, 33), (33, 17), (64, 64), (100, 30
 
 @pytest.mark.parametrize("m,n", SHAPES)
 @pytest.mark.parametrize("dtype", ["bf16", "f32"])
-@pytest.mark.parametrize("precond,iters", [("aol", 4), ("frobenius", 5), ("aol", 1)])
+@pytest.mark.parametrize("precond,iters", [("aol", 4), ("frobenius", 5), ("aol", 1),
+                                           ("schatten4", 4)])
 def test_shapes(m, n, dtype, precond, iters):
     log(f"case: {m}x{n} {dtype} {precond} t={iters}")
     X = make_input(m, n, 0.8, m * 7 + n, dtype)
@@ -66,7 +67,7 @@ def test_shapes(m, n, dtype, precond, iters):
 
 @pytest.mark.parametrize("m,n", [(17, 33), (33, 17), (256, 256), (100, 300), (300, 100)])
 @pytest.mark.parametrize("dtype", ["bf16", "f32"])
-@pytest.mark.parametrize("precond", ["aol", "frobenius"])
+@pytest.mark.parametrize("precond", ["aol", "frobenius", "schatten4"])
 def test_iters0_is_preconditioned_input(m, n, dtype, precond):
     log(f"case: iters=0 {m}x{n} {dtype} {precond}")
     X = make_input(m, n, 1.0, 3, dtype)
@@ -74,7 +75,7 @@ def test_iters0_is_preconditioned_input(m, n, dtype, precond):
     R = O.preconditioned(X, precond)
     assert relF(G, R) <= (4e-3 if dtype == "bf16" else 1e-6)
     u = 2.0 ** -8 if dtype == "bf16" else 2.0 ** -24
-    assert np.linalg.norm(G, 2) <= 1 + 4 * u   # AOL / Frobenius bound ||X1||_2 <= 1
+    assert np.linalg.norm(G, 2) <= 1 + 4 * u   # AOL / Frobenius / Schatten-4 bound ||X1||_2 <= 1
 
 
 def test_precond_none_and_iters0_none_is_identity():
@@ -103,7 +104,7 @@ def test_step_isolating_coefficients(coeffs, dtype, m, n):
 
 def test_zero_matrix_and_zero_row():
     for dtype in ("bf16", "f32"):
-        for pre in ("aol", "frobenius"):
+        for pre in ("aol", "frobenius", "schatten4"):
             Z = np.zeros((48, 80))
             assert np.all(gpu_orth(Z, dtype, 4, pre) == 0)
         X = make_input(48, 80, 1.0, 2, dtype)
@@ -169,3 +170,15 @@ def test_grouped_resnet_conv_64_matrices():
         worst = max(worst, e)
         assert e <= BF16_TOL and abs(r - 1) <= EO_RATIO_TOL, (i, e, r)
     log(f"worst relF={worst:.3e}")
+
+
+@pytest.mark.parametrize("m,n", [(768, 3072), (3072, 768)])
+def test_schatten4_gpt2_mlp_bf16(m, n):
+    log(f"case: {m}x{n} bf16 alpha=0.8 seed=0 schatten4 t=4")
+    X = make_input(m, n, 0.8, 0, "bf16")
+    G = gpu_orth(X, "bf16", 4, "schatten4")
+    R = O.orthogonalize(X, 4, None, "schatten4")
+    e, r = relF(G, R), eo_ratio(G, R)
+    log(f"relF={e:.3e} eo_ratio={r:.4f}")
+    assert e <= BF16_TOL
+    assert abs(r - 1) <= EO_RATIO_TOL
