@@ -184,6 +184,33 @@ struct Plan {
   hipStream_t st;
 };
 
+// Compute units of the MI355X: the blocks of one full wave of the large tiles.
+constexpr int kWave = 256;
+
+// Enqueue one kernel launch of a prepared phase descriptor (timed when the
+// timing hooks are on).
+tm_status fire(const Plan& pl, int kind, int cfg, const Phase& P) {
+  TimedLaunch tl{kind, nullptr, nullptr};
+  if (g_timing && P.total > 0) {
+    if (hipEventCreate(&tl.start) != hipSuccess || hipEventCreate(&tl.stop) != hipSuccess)
+      return fail(TM_ERR_HIP, "hipEventCreate failed");
+    (void)hipEventRecord(tl.start, pl.st);
+  }
+  hipError_t e;
+  if (pl.esz == 4)
+    e = tmk::launch_phase_f32(kind, cfg, P, pl.st);
+  else if (kind == tmk::kKindFrob || kind == tmk::kKindAolVector || kind == tmk::kKindApplyScale)
+    e = tmk::launch_elementwise_bf16(kind, P, pl.st);
+  else
+    e = tmk::launch_fast_bf16(kind, cfg, P, pl.st);
+  if (tl.start) {
+    (void)hipEventRecord(tl.stop, pl.st);
+    g_timed.push_back(tl);
+  }
+  if (e != hipSuccess) return fail(TM_ERR_HIP, std::string("kernel launch: ") + hipGetErrorString(e));
+  return TM_OK;
+}
+
 // One launch of `kind` per chunk of at most kMaxEntries items.
 tm_status launch(const Plan& pl, int kind, int cfg, int src, int dst, float a, float b, float c,
                  uint32_t flags, int aux, bool tall_only) {
@@ -222,30 +249,32 @@ tm_status launch(const Plan& pl, int kind, int cfg, int src, int dst, float a, f
     P.c = c;
     P.flags = flags;
     P.aux = aux;
-    TimedLaunch tl{kind, nullptr, nullptr};
-    if (g_timing && P.total > 0) {
-      if (hipEventCreate(&tl.start) != hipSuccess || hipEventCreate(&tl.stop) != hipSuccess)
-        return fail(TM_ERR_HIP, "hipEventCreate failed");
-      (void)hipEventRecord(tl.start, pl.st);
+    P.tail_base = 0;
+    tm_status s = TM_OK;
+    // bf16 Gram / polynomial on 256 x 256 tiles whose last wave would be at
+    // most half full: the full waves run as usual, the remaining tiles as
+    // 2 x 2 sub-tiles of 128 x 128 in a second launch (same per-element
+    // arithmetic, four times the blocks for the idle compute units).
+    const int tail = (pl.esz == 2 && cfg == 0 && (kind == tmk::kKindGram || kind == tmk::kKindPoly) &&
+                      P.total > kWave && P.total % kWave <= kWave / 2)
+                         ? P.total % kWave
+                         : 0;
+    if (tail > 0) {
+      P.total -= tail;
+      s = fire(pl, kind, cfg, P);
+      Phase Q = P;
+      Q.flags |= tmk::kTail;
+      Q.tail_base = P.total;
+      Q.total = 4 * tail;
+      if (s == TM_OK) s = fire(pl, kind, 1, Q);
+    } else {
+      s = fire(pl, kind, cfg, P);
     }
-    hipError_t e;
-    if (pl.esz == 4)
-      e = tmk::launch_phase_f32(kind, cfg, P, pl.st);
-    else if (kind == tmk::kKindFrob || kind == tmk::kKindAolVector || kind == tmk::kKindApplyScale)
-      e = tmk::launch_elementwise_bf16(kind, P, pl.st);
-    else
-      e = tmk::launch_fast_bf16(kind, cfg, P, pl.st);
-    if (tl.start) {
-      (void)hipEventRecord(tl.stop, pl.st);
-      g_timed.push_back(tl);
-    }
-    if (e != hipSuccess)
-      return fail(TM_ERR_HIP, std::string("kernel launch: ") + hipGetErrorString(e));
+    if (s != TM_OK) return s;
   }
   return TM_OK;
 }
 
-// bf16: zero-padded tiled workspace, matrix-core kernels of tm_fast.hip.
 // Scale vector s from the first Gram (its flags carry the row partials):
 // AOL (Algorithm 2, second line) s_i = 1 / sqrt(row sum of |A0|); Schatten-4
 // the uniform ||A0||_F^(-1/2), summed from the squares' row partials.  `part`

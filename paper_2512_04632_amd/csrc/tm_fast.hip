@@ -459,6 +459,28 @@ __device__ inline void tri_tile(int t, int nb, int& I, int& J) {
   J = I + t;
 }
 
+// Upper tile (I, J) of a symmetric product for this block.  Normally block
+// -> logical tile through the XCD mapping.  Under kTail the launch covers the
+// logical tiles (of size 2T) from P.tail_base on, four blocks per tile, one
+// per T x T sub-tile; the sub-tile below the diagonal of a diagonal tile has
+// no work (false).
+template <int T>
+__device__ inline bool sym_tile(const Phase& P, Loc& L, int& I, int& J) {
+  if (P.flags & kTail) {
+    const int sub = int(blockIdx.x) & 3;
+    L = locate(P, P.tail_base + int(blockIdx.x >> 2));
+    int I2, J2;
+    tri_tile(L.tile, int(P.e[L.ent].kp) / (2 * T), I2, J2);
+    if (I2 == J2 && sub == 2) return false;
+    I = 2 * I2 + (sub >> 1);
+    J = 2 * J2 + (sub & 1);
+    return true;
+  }
+  L = locate(P, xcd_remap(blockIdx.x, P.total));
+  tri_tile(L.tile, int(P.e[L.ent].kp) / T, I, J);
+  return true;
+}
+
 template <int T>
 __device__ inline int acc_row(int wm, int fm, int v) {
   return wm * Tile<T>::TWM + fm * 32 + 8 * (v >> 2) + 4 * ((threadIdx.x & 63) >> 5) + (v & 3);
@@ -649,11 +671,11 @@ template <int T>
 __global__ __launch_bounds__(Tile<T>::NT) void k_gram_fast(const Phase P) {
   __shared__ __attribute__((aligned(1024))) char smem[smem_bytes<T>()];
   constexpr int FM = Tile<T>::FM, FN = Tile<T>::FN;
-  const Loc L = locate(P, xcd_remap(blockIdx.x, P.total));
+  Loc L;
+  int I, J;
+  if (!sym_tile<T>(P, L, I, J)) return;
   const Entry& E = P.e[L.ent];
   const int kp = int(E.kp), Np = int(E.Np);
-  int I, J;
-  tri_tile(L.tile, kp / T, I, J);
   const uint16_t* Y = wbuf(P, E, L.mat, P.src);
   char* w = ws_of(P, E, L.mat);
   const WsLayout WL = ws_layout(E.kp, E.Np, 2);
@@ -672,10 +694,11 @@ __global__ __launch_bounds__(Tile<T>::NT) void k_gram_fast(const Phase P) {
     // part[b][i] = sum over the 64 columns of block b of |A0_ij| (with kRowSq:
     // A0_ij^2, whose total is ||A0||_F^2 for the Schatten-4 scale), from the fp32
     // accumulators.  The reduction tree is fixed for every tile size: each
-    // 32 x 32 MFMA block is reduced first (rows: across its 32 lanes; columns:
-    // over its 16 registers, then the lane pair), then two adjacent 32-blocks
-    // are added.  Off-diagonal tiles also emit the partials of the mirrored
-    // tile (column sums), so every row of A0 gets kp / 64 partials.
+    // 32 x 32 MFMA block is reduced first (a butterfly over its 32 columns for
+    // the row sums, the same pairing over its 32 rows for the column sums),
+    // then two adjacent 32-blocks are added.  Off-diagonal tiles also emit the
+    // partials of the mirrored tile (column sums), so every row of A0 gets
+    // kp / 64 partials, identical whichever tile size produced them.
     __syncthreads();
     float* part = reinterpret_cast<float*>(w + WL.part);
     const bool sq = (P.flags & kRowSq) != 0u;   // Schatten-4: sums of A0_ij^2
@@ -696,11 +719,20 @@ __global__ __launch_bounds__(Tile<T>::NT) void k_gram_fast(const Phase P) {
           for (int off = 16; off >= 1; off >>= 1) x += __shfl_xor(x, off, 64);
           if ((lane & 31) == 0) rs[((wn * Tile<T>::TWN) / 32 + fn) * T + acc_row<T>(wm, fm, v)] = x;
         }
-        float y = 0.f;
+        // Column sums with the pairing of the row butterfly above, applied to
+        // the row index 8 (v / 4) + 4 (lane / 32) + v % 4: bit 4 (v ^ 8),
+        // bit 3 (v ^ 4), bit 2 (the other lane half), bit 1, bit 0.  A column
+        // sum is then bit for bit the row sum of the transposed block, which
+        // the mirrored tile of a smaller tile size computes as a row sum.
+        float y[8];
 #pragma unroll
-        for (int v = 0; v < 16; ++v) y += mag(acc[fm][fn][v]);
-        y += __shfl_xor(y, 32, 64);
-        if (lane < 32) cs[((wm * Tile<T>::TWM) / 32 + fm) * T + acc_col<T>(wn, fn)] = y;
+        for (int v = 0; v < 8; ++v) y[v] = mag(acc[fm][fn][v]) + mag(acc[fm][fn][v + 8]);
+#pragma unroll
+        for (int v = 0; v < 4; ++v) y[v] += y[v + 4];
+#pragma unroll
+        for (int v = 0; v < 4; ++v) y[v] += __shfl_xor(y[v], 32, 64);
+        const float col = (y[0] + y[2]) + (y[1] + y[3]);
+        if (lane < 32) cs[((wm * Tile<T>::TWM) / 32 + fm) * T + acc_col<T>(wn, fn)] = col;
       }
     __syncthreads();
     constexpr int NB64 = T / 64;
@@ -719,11 +751,11 @@ template <int T>
 __global__ __launch_bounds__(Tile<T>::NT) void k_poly_fast(const Phase P) {
   __shared__ __attribute__((aligned(1024))) char smem[smem_bytes<T>()];
   constexpr int FM = Tile<T>::FM, FN = Tile<T>::FN;
-  const Loc L = locate(P, xcd_remap(blockIdx.x, P.total));
+  Loc L;
+  int I, J;
+  if (!sym_tile<T>(P, L, I, J)) return;
   const Entry& E = P.e[L.ent];
   const int kp = int(E.kp);
-  int I, J;
-  tri_tile(L.tile, kp / T, I, J);
   char* w = ws_of(P, E, L.mat);
   const WsLayout WL = ws_layout(E.kp, E.Np, 2);
   const uint16_t* A = reinterpret_cast<const uint16_t*>(w + WL.a);

@@ -43,6 +43,8 @@ constexpr uint32_t kA32 = 8u;     // Gram stores A0 in fp32 (first iteration, be
 constexpr uint32_t kRowSq = 16u;  // with kRowSum: partials of A0_ij^2 instead of |A0_ij|
 constexpr uint32_t kS4 = 32u;     // with kFrob: s = (sum of the partials)^(-1/4) (Schatten-4)
 constexpr uint32_t kFromPart = 64u;  // Frobenius-partial kernel sums the Gram's row partials
+constexpr uint32_t kTail = 128u;  // symmetric kernels: blocks are 2 x 2 sub-tiles of the
+                                  // tiles of twice their size from tail_base on
 
 // Entry flags.
 constexpr uint32_t kTall = 1u;    // the user matrix is N x k (m > n); work on its transpose
@@ -69,7 +71,8 @@ struct Phase {
   int32_t src, dst;    // Y slots
   float a, b, c;       // coefficients of this iteration
   uint32_t flags;
-  int32_t aux;         // AOL-vector kernel: tile size of the Gram that wrote the partials
+  int32_t aux;         // AOL-vector / partial kernels: columns per row partial of the Gram
+  int32_t tail_base;   // with kTail: first logical tile (of size 2T) covered by the launch
 };
 
 // Tile configurations of the matrix-core kernels (square tiles, 256 threads).

@@ -1,0 +1,57 @@
+"""Full-size batches through the C ABI, in the launch configuration the
+benchmark times.
+
+At these sizes the Gram and polynomial phases run on 256 x 256 tiles with the
+last, partly filled wave split into 128 x 128 sub-tiles, while a single matrix
+of the same shape runs them on 128 x 128 tiles throughout.  Every output
+element accumulates the same products in the same order either way, so a
+matrix must come out of the batched call bit for bit as from its own call.
+Matrix 0 of the 8 x 4096 x 14336 batch is checked against the fp64 oracle.
+"""
+import numpy as np
+import pytest
+
+from oracle import turbomuon as O
+from paper_2512_04632_amd import synth
+from gpu_helpers import BF16_TOL, EO_RATIO_TOL, from_device, log
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+from paper_2512_04632_amd import _lib as tm  # noqa: E402
+
+
+def _single(x):
+    t = x.clone().contiguous()
+    tm.orthogonalize(t, 4, None, "aol")
+    return t
+
+
+def test_llm8b_4096x14336_batch_of_8():
+    log("case: 8 x 4096 x 14336 bf16 power law alpha=0.5 seed=0, batched AOL t=4")
+    X = synth.power_law_batch_device(8, 4096, 14336, 0.5, seed=0, device="cuda")
+    torch.cuda.synchronize()
+    x0 = from_device(X[0])
+    B = X.clone()
+    tm.orthogonalize(B, 4, None, "aol")
+    S7 = _single(X[7])
+    torch.cuda.synchronize()
+    assert torch.equal(B[7], S7)
+    G = from_device(B[0])
+    R = O.orthogonalize(x0, 4, None, "aol")
+    e, r = O.rel_frobenius(G, R), O.eps_ortho(G) / O.eps_ortho(R)
+    log(f"matrix 0: relF={e:.3e} eps_ortho ratio={r:.4f}")
+    assert e <= BF16_TOL and abs(r - 1) <= EO_RATIO_TOL
+    assert torch.isfinite(B.float()).all()
+
+
+def test_square_4096_batch_of_4_matches_single_calls():
+    log("case: 4 x 4096 x 4096 bf16 N(0,1) seed=1, batched vs single AOL t=4")
+    g = torch.Generator(device="cuda")
+    g.manual_seed(1)
+    X = torch.randn((4, 4096, 4096), generator=g, device="cuda").to(torch.bfloat16)
+    B = X.clone()
+    tm.orthogonalize(B, 4, None, "aol")
+    for i in range(4):
+        assert torch.equal(B[i], _single(X[i])), i
+    torch.cuda.synchronize()
