@@ -79,7 +79,11 @@ struct Item {
   uint32_t kp, Np;     // padded workspace dims (set by the planner)
   uint32_t count;
   bool tall;
+  bool direct;         // bf16: iteration 1 reads the caller's matrix in place of a padded copy
 };
+
+// Which items a launch covers (the others get no blocks).
+enum Cover { kCoverAll, kCoverTall, kCoverCopied };
 
 tm_status check_device(int* dev) {
   hipError_t e = hipGetDevice(dev);
@@ -213,7 +217,7 @@ tm_status fire(const Plan& pl, int kind, int cfg, const Phase& P) {
 
 // One launch of `kind` per chunk of at most kMaxEntries items.
 tm_status launch(const Plan& pl, int kind, int cfg, int src, int dst, float a, float b, float c,
-                 uint32_t flags, int aux, bool tall_only) {
+                 uint32_t flags, int aux, Cover cover = kCoverAll) {
   const std::vector<Item>& items = *pl.items;
   for (size_t base = 0; base < items.size(); base += tmk::kMaxEntries) {
     Phase P;
@@ -230,11 +234,10 @@ tm_status launch(const Plan& pl, int kind, int cfg, int src, int dst, float a, f
       E.kp = it.kp;
       E.Np = it.Np;
       E.count = it.count;
-      E.flags = it.tall ? tmk::kTall : 0u;
+      E.flags = (it.tall ? tmk::kTall : 0u) | (it.direct ? tmk::kDirect : 0u);
       E.tile_start = uint32_t(start);
-      E.tiles_per = (tall_only && !it.tall)
-                        ? 0u
-                        : tmk::blocks_per_matrix(kind, cfg, it.k, it.N, it.kp, it.Np);
+      const bool skip = (cover == kCoverTall && !it.tall) || (cover == kCoverCopied && it.direct);
+      E.tiles_per = skip ? 0u : tmk::blocks_per_matrix(kind, cfg, it.k, it.N, it.kp, it.Np);
       start += uint64_t(E.tiles_per) * it.count;
     }
     if (start >= (uint64_t(1) << 31))
@@ -281,10 +284,10 @@ tm_status launch(const Plan& pl, int kind, int cfg, int src, int dst, float a, f
 // is the column granularity of the row partials.
 tm_status gram_scale(const Plan& pl, int precond, int part) {
   if (precond == TM_PRECOND_AOL)
-    return launch(pl, tmk::kKindAolVector, 0, 0, 0, 0.f, 0.f, 0.f, 0u, part, false);
-  tm_status s = launch(pl, tmk::kKindFrob, 0, 0, 0, 0.f, 0.f, 0.f, tmk::kFromPart, part, false);
+    return launch(pl, tmk::kKindAolVector, 0, 0, 0, 0.f, 0.f, 0.f, 0u, part);
+  tm_status s = launch(pl, tmk::kKindFrob, 0, 0, 0, 0.f, 0.f, 0.f, tmk::kFromPart, part);
   if (s == TM_OK)
-    s = launch(pl, tmk::kKindAolVector, 0, 0, 0, 0.f, 0.f, 0.f, tmk::kFrob | tmk::kS4, 0, false);
+    s = launch(pl, tmk::kKindAolVector, 0, 0, 0, 0.f, 0.f, 0.f, tmk::kFrob | tmk::kS4, 0);
   return s;
 }
 
@@ -305,20 +308,20 @@ tm_status plan_bf16(const Plan& pl, int iters, const float* coeffs, int precond,
   const int pcfg = choose_sym_cfg(tmk::kKindPoly, tcfg, *pl.items);
   const int part = tmk::kMinTile;   // the matrix-core Gram emits row partials per 64 columns
   tm_status s = TM_OK;
-  if (iters > 0 || from_gram) s = launch(pl, tmk::kKindLoadIn, 0, 0, 0, 0.f, 0.f, 0.f, 0u, 0, false);
+  if (iters > 0 || from_gram)
+    s = launch(pl, tmk::kKindLoadIn, 0, 0, 0, 0.f, 0.f, 0.f, 0u, 0, kCoverCopied);
   if (s == TM_OK && frob) {  // Algorithm 1, first line: s = 1 / ||X0||_F
-    s = launch(pl, tmk::kKindFrob, 0, 0, 0, 0.f, 0.f, 0.f, 0u, 0, false);
-    if (s == TM_OK) s = launch(pl, tmk::kKindAolVector, 0, 0, 0, 0.f, 0.f, 0.f, tmk::kFrob, 0, false);
+    s = launch(pl, tmk::kKindFrob, 0, 0, 0, 0.f, 0.f, 0.f, 0u, 0);
+    if (s == TM_OK) s = launch(pl, tmk::kKindAolVector, 0, 0, 0, 0.f, 0.f, 0.f, tmk::kFrob, 0);
   }
   if (s != TM_OK) return s;
   if (iters == 0) {
     if (from_gram) {
-      s = launch(pl, tmk::kKindGram, gcfg, tmk::kSlotFirst, 0, 0.f, 0.f, 0.f, rflags | tmk::kA32, 0,
-                 false);
+      s = launch(pl, tmk::kKindGram, gcfg, tmk::kSlotFirst, 0, 0.f, 0.f, 0.f, rflags | tmk::kA32, 0);
       if (s == TM_OK) s = gram_scale(pl, precond, part);
       if (s != TM_OK) return s;
     }
-    if (scaled) s = launch(pl, tmk::kKindApplyScale, 0, 0, 0, 0.f, 0.f, 0.f, 0u, 0, false);
+    if (scaled) s = launch(pl, tmk::kKindApplyScale, 0, 0, 0, 0.f, 0.f, 0.f, 0u, 0);
     return s;
   }
   int src = tmk::kSlotFirst;
@@ -330,12 +333,12 @@ tm_status plan_bf16(const Plan& pl, int iters, const float* coeffs, int precond,
     const bool first = it == 1;
     const uint32_t scale = (first && scaled) ? tmk::kScale : 0u;
     const uint32_t gflags = (first ? rflags : 0u) | (scale ? tmk::kA32 : 0u);
-    s = launch(pl, tmk::kKindGram, gcfg, src, 0, 0.f, 0.f, 0.f, gflags, 0, false);
+    s = launch(pl, tmk::kKindGram, gcfg, src, 0, 0.f, 0.f, 0.f, gflags, 0);
     if (s == TM_OK && first && from_gram) s = gram_scale(pl, precond, part);
     if (s == TM_OK && scale)         // A1 = diag(s) A0 diag(s), one rounding
-      s = launch(pl, tmk::kKindScaleA, 0, 0, 0, 0.f, 0.f, 0.f, 0u, 0, false);
-    if (s == TM_OK) s = launch(pl, tmk::kKindPoly, pcfg, 0, 0, a, b, c, scale, 0, false);
-    if (s == TM_OK) s = launch(pl, tmk::kKindUpdate, tcfg, src, dst, a, b, c, scale, 0, false);
+      s = launch(pl, tmk::kKindScaleA, 0, 0, 0, 0.f, 0.f, 0.f, 0u, 0);
+    if (s == TM_OK) s = launch(pl, tmk::kKindPoly, pcfg, 0, 0, a, b, c, scale, 0);
+    if (s == TM_OK) s = launch(pl, tmk::kKindUpdate, tcfg, src, dst, a, b, c, scale, 0);
     src = dst;
   }
   return s;
@@ -352,7 +355,7 @@ tm_status plan_f32(const Plan& pl, int iters, const float* coeffs, int precond) 
   bool any_tall = false;
   for (const Item& it : items) any_tall = any_tall || it.tall;
   if (any_tall && (iters > 0 || from_gram)) {
-    s = launch(pl, tmk::kKindTransposeIn, 0, 0, 0, 0.f, 0.f, 0.f, 0u, 0, true);
+    s = launch(pl, tmk::kKindTransposeIn, 0, 0, 0, 0.f, 0.f, 0.f, 0u, 0, kCoverTall);
     if (s != TM_OK) return s;
   }
   const int gcfg = choose_cfg(tmk::kKindGram, items);
@@ -361,18 +364,17 @@ tm_status plan_f32(const Plan& pl, int iters, const float* coeffs, int precond) 
   const int part = tmk::cfg_tile(gcfg);   // row partials per Gram tile column block
 
   if (frob) {  // Algorithm 1, first line: s = 1 / ||X0||_F
-    s = launch(pl, tmk::kKindFrob, 0, 0, 0, 0.f, 0.f, 0.f, 0u, 0, false);
-    if (s == TM_OK) s = launch(pl, tmk::kKindAolVector, 0, 0, 0, 0.f, 0.f, 0.f, tmk::kFrob, 0, false);
+    s = launch(pl, tmk::kKindFrob, 0, 0, 0, 0.f, 0.f, 0.f, 0u, 0);
+    if (s == TM_OK) s = launch(pl, tmk::kKindAolVector, 0, 0, 0, 0.f, 0.f, 0.f, tmk::kFrob, 0);
     if (s != TM_OK) return s;
   }
   if (iters == 0) {
     if (from_gram) {
-      s = launch(pl, tmk::kKindGram, gcfg, tmk::kSlotFirst, 0, 0.f, 0.f, 0.f, rflags | tmk::kA32, 0,
-                 false);
+      s = launch(pl, tmk::kKindGram, gcfg, tmk::kSlotFirst, 0, 0.f, 0.f, 0.f, rflags | tmk::kA32, 0);
       if (s == TM_OK) s = gram_scale(pl, precond, part);
       if (s != TM_OK) return s;
     }
-    if (scaled) s = launch(pl, tmk::kKindApplyScale, 0, 0, 0, 0.f, 0.f, 0.f, 0u, 0, false);
+    if (scaled) s = launch(pl, tmk::kKindApplyScale, 0, 0, 0, 0.f, 0.f, 0.f, 0u, 0);
     return s;
   }
 
@@ -388,14 +390,14 @@ tm_status plan_f32(const Plan& pl, int iters, const float* coeffs, int precond) 
     const bool first = it == 1;
     const uint32_t scale = (first && scaled) ? tmk::kScale : 0u;
     const uint32_t gflags = (first ? rflags : 0u) | (scale ? tmk::kA32 : 0u);
-    s = launch(pl, tmk::kKindGram, gcfg, src, 0, 0.f, 0.f, 0.f, gflags, 0, false);
+    s = launch(pl, tmk::kKindGram, gcfg, src, 0, 0.f, 0.f, 0.f, gflags, 0);
     if (s == TM_OK && first && from_gram) s = gram_scale(pl, precond, part);
-    if (s == TM_OK) s = launch(pl, tmk::kKindPoly, pcfg, 0, 0, a, b, c, scale, 0, false);
-    if (s == TM_OK) s = launch(pl, tmk::kKindUpdate, ucfg, src, dst, a, b, c, scale, 0, false);
+    if (s == TM_OK) s = launch(pl, tmk::kKindPoly, pcfg, 0, 0, a, b, c, scale, 0);
+    if (s == TM_OK) s = launch(pl, tmk::kKindUpdate, ucfg, src, dst, a, b, c, scale, 0);
     if (s != TM_OK) return s;
     src = dst;
   }
-  if (iters == 1) s = launch(pl, tmk::kKindCopyOut, 0, src, 0, 0.f, 0.f, 0.f, 0u, 0, false);
+  if (iters == 1) s = launch(pl, tmk::kKindCopyOut, 0, src, 0, 0.f, 0.f, 0.f, 0u, 0);
   return s;
 }
 
@@ -409,7 +411,14 @@ tm_status run(std::vector<Item>& items, int esz, int iters, const float* coeffs,
   int tcfg = 0;
   if (esz == 2) {
     tcfg = choose_tile_cfg(items);
-    for (Item& it : items) tmk::tiled_dims(it.k, it.N, uint32_t(tmk::cfg_tile(tcfg)), &it.kp, &it.Np);
+    for (Item& it : items) {
+      tmk::tiled_dims(it.k, it.N, uint32_t(tmk::cfg_tile(tcfg)), &it.kp, &it.Np);
+      // A wide matrix that needs no padding is read in place by iteration 1
+      // (and scaled there in place); a single iteration would read and write
+      // the caller's buffer in the same launch, so it keeps the copy.
+      it.direct = !it.tall && it.kp == it.k && it.Np == it.N && iters != 1 &&
+                  (reinterpret_cast<uintptr_t>(it.x) & 15u) == 0u;
+    }
   } else {
     for (Item& it : items) tmk::generic_dims(it.k, it.N, &it.kp, &it.Np);
   }
@@ -448,6 +457,7 @@ Item make_item(void* X, int64_t m, int64_t n, int64_t count) {
   Item it;
   it.x = static_cast<char*>(X);
   it.tall = m > n;
+  it.direct = false;
   it.k = uint32_t(std::min(m, n));
   it.N = uint32_t(std::max(m, n));
   it.kp = it.k;

@@ -442,9 +442,12 @@ __device__ inline uint16_t* user_of(const Entry& E, int mat) {
   return reinterpret_cast<uint16_t*>(E.x + uint64_t(mat) * E.k * E.N * 2u);
 }
 
-// Workspace Y buffer of a slot (kp x Np, ld ldy): the first slot is W1, then
-// W2, W1, ... (the final slot is the caller's matrix, handled by the update).
+// Y buffer of a slot (kp x Np, ld ldy): the first slot is W1 (or, for a
+// kDirect entry, the caller's matrix, which then has exactly that layout),
+// then W2, W1, ... (the final slot is the caller's matrix, handled by the
+// update).
 __device__ inline uint16_t* wbuf(const Phase& P, const Entry& E, int mat, int slot) {
+  if (slot == kSlotFirst && (E.flags & kDirect)) return user_of(E, mat);
   const WsLayout L = ws_layout(E.kp, E.Np, 2);
   const bool w1 = slot == kSlotFirst || slot == kSlotAlt2;
   return reinterpret_cast<uint16_t*>(ws_of(P, E, mat) + (w1 ? L.w1 : L.w2));
@@ -875,7 +878,7 @@ __global__ __launch_bounds__(256) void k_load_in(const Phase P) {
 }
 
 // First iteration after AOL / Frobenius scaling: A1 = bf16(s_i A0_ij s_j)
-// over the padded kp x kp square and X1 = bf16(s_i X0_il) in place on W1;
+// over the padded kp x kp square and X1 = bf16(s_i X0_il) in place on slot 0;
 // 8 elements per thread, the A blocks first.
 __global__ __launch_bounds__(256) void k_apply_s(const Phase P) {
   const Loc L = locate(P, blockIdx.x);
@@ -901,7 +904,7 @@ __global__ __launch_bounds__(256) void k_apply_s(const Phase P) {
   const int64_t idx = int64_t(L.tile - nA) * kElemBlock + int64_t(threadIdx.x) * 8;
   if (idx >= kp * Np) return;
   const int64_t i = idx / Np, l = idx - i * Np;   // Np % 8 == 0: the 8 stay in row i
-  uint16_t* Y = reinterpret_cast<uint16_t*>(w + WL.w1) + i * WL.ldy + l;
+  uint16_t* Y = wbuf(P, E, L.mat, kSlotFirst) + i * WL.ldy + l;
   const float si = s[i];
   uint4 v = *reinterpret_cast<const uint4*>(Y);
   uint16_t* e = reinterpret_cast<uint16_t*>(&v);

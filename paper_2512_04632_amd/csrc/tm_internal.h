@@ -28,6 +28,9 @@ constexpr int kMaxEntries = 64;
 //   1      W1                     W2
 //   2      W2                     W1
 //   3      user matrix            user matrix, stored transposed (N x k, ld = k)
+// (fp32 path; the bf16 path pads every matrix into W1 = slot 0 first, W2 and
+// W1 being slots 1 and 2, unless the entry is kDirect: then slot 0 is the
+// user matrix itself.)
 // Iteration 1 reads slot 0, iterations write 1, 2, 1, 2, ... and the last
 // one writes slot 3, so no update ever reads the buffer it writes.
 constexpr int kSlotFirst = 0;
@@ -48,6 +51,9 @@ constexpr uint32_t kTail = 128u;  // symmetric kernels: blocks are 2 x 2 sub-til
 
 // Entry flags.
 constexpr uint32_t kTall = 1u;    // the user matrix is N x k (m > n); work on its transpose
+constexpr uint32_t kDirect = 2u;  // bf16: the user matrix already has the padded layout (wide,
+                                  // dims multiples of the tile, 16-byte aligned); iteration 1
+                                  // reads it in place of the W1 copy
 
 constexpr int kFrobBlocks = 32;   // partial sums of squares per matrix
 constexpr int kMinTile = 64;      // smallest Gram tile: bounds the row-sum partial count

@@ -182,3 +182,25 @@ def test_schatten4_gpt2_mlp_bf16(m, n):
     log(f"relF={e:.3e} eo_ratio={r:.4f}")
     assert e <= BF16_TOL
     assert abs(r - 1) <= EO_RATIO_TOL
+
+
+@pytest.mark.parametrize("m,n", [(256, 512), (768, 3072)])
+@pytest.mark.parametrize("precond,iters", [("aol", 4), ("frobenius", 5), ("schatten4", 2),
+                                           ("none", 3), ("aol", 0), ("aol", 1)])
+def test_in_place_first_iteration_matches_padded_copy(m, n, precond, iters):
+    """A wide matrix whose dims are multiples of the tile is read in place by the
+    first iteration when 16-byte aligned; one stored 2 bytes past an alignment
+    boundary goes through the padded copy.  Same arithmetic, same bits."""
+    log(f"case: in-place vs copied first iteration {m}x{n} {precond} t={iters}")
+    X = make_input(m, n, 0.8, 9, "bf16")
+    a = to_device(X, "bf16")
+    buf = torch.empty(m * n + 8, dtype=torch.bfloat16, device="cuda")
+    b = buf[1:1 + m * n].view(m, n)
+    b.copy_(a)
+    assert a.data_ptr() % 16 == 0 and b.data_ptr() % 16 == 2
+    tm.orthogonalize(a, iters, None, precond)
+    tm.orthogonalize(b, iters, None, precond)
+    torch.cuda.synchronize()
+    assert torch.equal(a, b)
+    R = O.orthogonalize(X, iters, None, precond)
+    assert relF(from_device(a), R) <= (4e-3 if iters == 0 else BF16_TOL)
