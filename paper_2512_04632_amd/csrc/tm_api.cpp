@@ -254,12 +254,12 @@ tm_status launch(const Plan& pl, int kind, int cfg, int src, int dst, float a, f
     P.aux = aux;
     P.tail_base = 0;
     tm_status s = TM_OK;
-    // bf16 Gram / polynomial on 256 x 256 tiles whose last wave would be at
-    // most half full: the full waves run as usual, the remaining tiles as
-    // 2 x 2 sub-tiles of 128 x 128 in a second launch (same per-element
-    // arithmetic, four times the blocks for the idle compute units).
-    const int tail = (pl.esz == 2 && cfg == 0 && (kind == tmk::kKindGram || kind == tmk::kKindPoly) &&
-                      P.total > kWave && P.total % kWave <= kWave / 2)
+    // bf16 matrix-core phases on 256 x 256 tiles whose last wave would be at
+    // most a quarter full: the full waves run as usual, the remaining tiles as
+    // 2 x 2 sub-tiles of 128 x 128 in a second launch that fits in one wave
+    // (same per-element arithmetic, four times the blocks for the idle units).
+    const bool mc = kind == tmk::kKindGram || kind == tmk::kKindPoly || kind == tmk::kKindUpdate;
+    const int tail = (pl.esz == 2 && cfg == 0 && mc && P.total > kWave && P.total % kWave <= kWave / 4)
                          ? P.total % kWave
                          : 0;
     if (tail > 0) {

@@ -46,7 +46,7 @@ constexpr uint32_t kA32 = 8u;     // Gram stores A0 in fp32 (first iteration, be
 constexpr uint32_t kRowSq = 16u;  // with kRowSum: partials of A0_ij^2 instead of |A0_ij|
 constexpr uint32_t kS4 = 32u;     // with kFrob: s = (sum of the partials)^(-1/4) (Schatten-4)
 constexpr uint32_t kFromPart = 64u;  // Frobenius-partial kernel sums the Gram's row partials
-constexpr uint32_t kTail = 128u;  // symmetric kernels: blocks are 2 x 2 sub-tiles of the
+constexpr uint32_t kTail = 128u;  // matrix-core kernels: blocks are 2 x 2 sub-tiles of the
                                   // tiles of twice their size from tail_base on
 
 // Entry flags.

@@ -158,6 +158,21 @@ def test_grouped_gpt2_small_72_matrices():
     log(f"worst relF={worst:.3e}")
 
 
+def test_grouped_gpt2_small_matches_single_calls_bitwise():
+    """The grouped call runs 256-tiles (its last update tiles, those of the last tall
+    matrix, as 128 x 128 sub-tiles); a single 3072 x 768 call runs 64-tiles.  Every
+    output element sees the same products in the same order: equal bits."""
+    log("case: grouped gpt2_small_12layer vs single calls, bitwise")
+    shapes = synth.workload_shapes("gpt2_small_12layer")
+    Xs = [make_input(m, n, a, s, "bf16") for (m, n, a, s) in shapes]
+    ts = [to_device(X, "bf16") for X in Xs]
+    tm.orthogonalize_grouped(ts, 4, None, "aol")
+    for i in (0, 47, 48, 59, 60, 71):
+        assert torch.equal(ts[i], (lambda t: (tm.orthogonalize(t, 4, None, "aol"), t)[1])(
+            to_device(Xs[i], "bf16"))), i
+    torch.cuda.synchronize()
+
+
 def test_grouped_resnet_conv_64_matrices():
     log("case: grouped resnet_conv_64 (64 matrices)")
     Xs, Gs = run_workload("resnet_conv_64")
