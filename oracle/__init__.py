@@ -7,5 +7,5 @@ calls it and shares no code with it.
 from .turbomuon import (  # noqa: F401
     CONSTANT_TRIPLE, aol_vector, aol, frobenius_scale, schatten4_scale, newton_schulz_alg2,
     orthogonalize, polar_factor, eps_ortho, eps_polar, eps_bias, eps_approx,
-    rel_frobenius, preconditioned,
+    rel_frobenius, preconditioned, round_bf16, muon_step,
 )

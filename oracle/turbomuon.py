@@ -210,3 +210,53 @@ def rel_frobenius(Z: np.ndarray, R: np.ndarray) -> float:
     d = np.linalg.norm(np.asarray(Z, dtype=np.float64) - R)
     r = np.linalg.norm(R)
     return float(d / r) if r > 0 else float(d)
+
+
+# ---------------------------------------------------------------------------
+# Optimizer step around the orthogonalization
+# ---------------------------------------------------------------------------
+
+def round_bf16(x: np.ndarray) -> np.ndarray:
+    """Round float64 values to the nearest bfloat16 (ties to even), as float64.
+
+    Written out on the bit pattern of the float32 value: keep the top 16 bits,
+    adding half an ulp of the kept part plus its lowest bit (round half to even).
+    """
+    f = np.ascontiguousarray(x, dtype=np.float32)
+    b = f.view(np.uint32).astype(np.uint64)
+    b = ((b + 0x7FFF + ((b >> 16) & 1)) >> 16) << 16
+    out = b.astype(np.uint32).view(np.float32).astype(np.float64)
+    out[np.isnan(f)] = np.nan
+    return out
+
+
+def muon_step(W: np.ndarray, G: np.ndarray, M: np.ndarray, lr: float, momentum: float,
+              nesterov: bool = True, weight_decay: float = 0.0, t: int = 4, coeffs=None,
+              precond: str = "aol", shape_scale: bool = True):
+    """One step of Muon with the orthogonalization replaced by this method.
+
+    The paper uses Turbo-Muon as a drop-in replacement of Muon's
+    orthogonalization and keeps the rest of Muon's step; that step is read as
+    heavy-ball momentum on the gradient, optionally in Nesterov form, followed
+    by the orthogonalized update (the steepest-descent appendix writes the
+    update as -eta PolarFactor(G S)):
+
+        M' = momentum M + G
+        U  = G + momentum M'   (nesterov)   or   U = M'
+        O  = orthogonalize(bf16(U), t, coeffs, precond)
+        W' = W (1 - lr weight_decay) - lr scale O,
+             scale = sqrt(max(1, rows / cols)) if shape_scale else 1.
+
+    U is rounded to bfloat16 first because that is the storage the
+    orthogonalization runs in.  Returns (W', M', O).
+    """
+    W = np.asarray(W, dtype=np.float64)
+    G = np.asarray(G, dtype=np.float64)
+    M = np.asarray(M, dtype=np.float64)
+    Mn = momentum * M + G
+    U = G + momentum * Mn if nesterov else Mn
+    O = orthogonalize(round_bf16(U), t, coeffs, precond)
+    m, n = W.shape
+    scale = np.sqrt(max(1.0, m / n)) if shape_scale else 1.0
+    Wn = W * (1.0 - lr * weight_decay) - lr * scale * O
+    return Wn, Mn, O

@@ -346,3 +346,72 @@ def test_schatten4_initial_polar_error_ordering(n):
         Q = O.polar_factor(X)
         e = {p: O.eps_polar(O.preconditioned(X, p), X, Q) for p in ("frobenius", "schatten4", "aol")}
         assert e["aol"] < e["schatten4"] < e["frobenius"]
+
+
+# --------------------------------------------------------------------------
+# Optimizer step around the orthogonalization (Muon's step, orthogonalization replaced)
+# --------------------------------------------------------------------------
+def test_round_bf16_matches_the_storage_rounding():
+    """The oracle's bf16 rounding equals an independent route: float32 -> bfloat16
+    through NumPy's round-half-even on the scaled mantissa, and exact values stay."""
+    rng = np.random.default_rng(0)
+    x = np.concatenate([rng.standard_normal(20000) * 10.0 ** rng.integers(-20, 20, 20000),
+                        [0.0, -0.0, 1.0, -2.5, 1.0 + 2.0 ** -8, 1.0 + 3 * 2.0 ** -9]])
+    got = O.round_bf16(x)
+    f = x.astype(np.float32).astype(np.float64)
+    e = np.floor(np.log2(np.abs(np.where(f == 0, 1.0, f))))
+    q = 2.0 ** (e - 7)                                   # bf16 ulp for a normal value
+    want = np.where(f == 0, f, np.round(f / q) * q)      # np.round: half to even
+    assert np.array_equal(got, want)
+    assert O.round_bf16(np.array([1.0 + 2.0 ** -8]))[0] == 1.0          # tie to even
+    assert O.round_bf16(np.array([1.0 + 3 * 2.0 ** -8]))[0] == 1.0 + 2.0 ** -6
+
+
+def test_muon_momentum_is_a_geometric_series():
+    """Constant gradient G from M = 0: after k steps M_k = G (1 - mu^k) / (1 - mu)."""
+    G = synth.power_law_matrix(12, 20, 0.8, seed=1)
+    W, M = np.zeros_like(G), np.zeros_like(G)
+    mu = 0.9
+    for k in range(1, 6):
+        W, M, _ = O.muon_step(W, G, M, lr=0.01, momentum=mu, nesterov=False)
+        assert np.max(np.abs(M - G * (1 - mu ** k) / (1 - mu))) <= 1e-13
+
+
+def test_muon_nesterov_two_steps_by_hand():
+    """Nesterov from M = 0: U1 = (1 + mu) G1; M1 = G1; U2 = G2 + mu (mu G1 + G2)."""
+    G1 = synth.power_law_matrix(10, 16, 1.0, seed=2)
+    G2 = synth.power_law_matrix(10, 16, 1.0, seed=3)
+    mu, lr = 0.95, 0.1
+    W0 = np.zeros_like(G1)
+    W1, M1, O1 = O.muon_step(W0, G1, np.zeros_like(G1), lr, mu, nesterov=True)
+    assert np.allclose(O1, O.orthogonalize(O.round_bf16((1 + mu) * G1), 4), rtol=0, atol=1e-14)
+    W2, M2, O2 = O.muon_step(W1, G2, M1, lr, mu, nesterov=True)
+    assert np.max(np.abs(M2 - (mu * G1 + G2))) <= 1e-14
+    assert np.allclose(O2, O.orthogonalize(O.round_bf16(G2 + mu * (mu * G1 + G2)), 4), rtol=0, atol=1e-14)
+    assert np.max(np.abs(W2 - (-lr * O1 - lr * O2))) <= 1e-14          # 10 x 16: scale 1
+
+
+def test_muon_weight_decay_and_shape_scale():
+    W = synth.power_law_matrix(30, 10, 1.0, seed=4)                      # tall: scale sqrt(3)
+    Z = np.zeros_like(W)
+    Wn, Mn, On = O.muon_step(W, Z, Z, lr=0.5, momentum=0.9, weight_decay=0.1)
+    assert np.all(On == 0) and np.all(Mn == 0)
+    assert np.max(np.abs(Wn - 0.95 * W)) <= 1e-15
+    G = synth.power_law_matrix(30, 10, 1.0, seed=5)
+    W1, _, O1 = O.muon_step(Z, G, Z, lr=1.0, momentum=0.0, nesterov=False)
+    assert np.max(np.abs(W1 + np.sqrt(3.0) * O1)) <= 1e-14
+    W2, _, _ = O.muon_step(Z, G, Z, lr=1.0, momentum=0.0, nesterov=False, shape_scale=False)
+    assert np.max(np.abs(W2 + O1)) <= 1e-14
+    # decoupled decay shrinks the old weights only, not the new step
+    W3, _, O3 = O.muon_step(W, G, Z, lr=0.5, momentum=0.0, nesterov=False, weight_decay=0.1)
+    assert np.max(np.abs(W3 - (0.95 * W - 0.5 * np.sqrt(3.0) * O3))) <= 1e-14
+    assert np.max(np.abs(W3 - 0.95 * (W - 0.5 * np.sqrt(3.0) * O3))) > 1e-3
+
+
+@pytest.mark.parametrize("seed", range(3))
+def test_muon_step_is_a_descent_direction(seed):
+    """Without momentum the step -lr O satisfies <G, W - W'> > 0 (Lemma 1's alignment)."""
+    G = np.random.default_rng(seed).standard_cauchy((24, 40))
+    W = np.zeros_like(G)
+    Wn, _, _ = O.muon_step(W, G, np.zeros_like(G), lr=0.1, momentum=0.0, nesterov=False)
+    assert np.sum(G * (W - Wn)) > 0
