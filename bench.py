@@ -54,6 +54,10 @@ def main(argv=None) -> int:
     ap.add_argument("--copy-calibration-mb", type=int, default=0,
                     help="after the timed region, run one plain device copy of this many MiB "
                          "(reference kernel for scaling the FETCH_SIZE / WRITE_SIZE counters)")
+    ap.add_argument("--optimizer", action="store_true",
+                    help="time the optimizer step (tm_muon_step_grouped: momentum, bf16 "
+                         "orthogonalization, fp32 parameter update) over the workload's matrices "
+                         "instead of the orthogonalization alone")
     ap.add_argument("--inputs", default="powerlaw", choices=["powerlaw", "gaussian"],
                     help="powerlaw: the seeded power-law-plus-noise recipe (QR on the GPU); "
                          "gaussian: i.i.d. N(0,1) entries, the paper's own synthetic law "
@@ -99,6 +103,9 @@ def main(argv=None) -> int:
         batches.append(X)
     torch.cuda.synchronize()
     n_mat = sum(c for c, _, _, _ in entries)
+
+    if args.optimizer:
+        return _bench_optimizer(args, batches, entries, dev, stream, progress)
 
     def run(bs):
         if grouped:
@@ -229,6 +236,58 @@ def main(argv=None) -> int:
     traffic = _recorded_traffic(upd_flops_per_launch) if args.workload == DEFAULT_WORKLOAD else None
     if traffic is not None:
         result["roofline"]["traffic"] = traffic
+    print(json.dumps(result), flush=True)
+    return 0
+
+
+def _bench_optimizer(args, batches, entries, dev, stream, progress):
+    """Optimizer steps/s over fp32 parameters shaped like the workload's matrices."""
+    import torch
+
+    from paper_2512_04632_amd import _lib as tm
+    g = torch.Generator(device=dev)
+    g.manual_seed(1)
+    grads = [X[i].float().contiguous() for X in batches for i in range(X.shape[0])]
+    params = [0.02 * torch.randn(t.shape, generator=g, device=dev) for t in grads]
+    bufs = [torch.zeros_like(t) for t in grads]
+    lr, mu = 0.02, 0.95
+
+    def step():
+        tm.muon_step_grouped(params, grads, bufs, lr, mu, True, 0.0, True, args.iters, None,
+                             args.precond)
+
+    progress(f"optimizer warmup {args.warmup}")
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    tm.timing_reset()
+    tm.timing_enable(True)
+    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    start.record(stream)
+    for _ in range(args.steps):
+        step()
+    stop.record(stream)
+    torch.cuda.synchronize()
+    tm.timing_enable(False)
+    ms = start.elapsed_time(stop) / args.steps
+    names = ("opt_momentum", "load_in", "gram", "aol_vector", "scale_a", "poly", "update",
+             "opt_apply")
+    phases = {p: round(tm.timing_read(p)[0] / args.steps, 4) for p in names}
+    n_el = sum(t.numel() for t in grads)
+    result = {
+        "metric": f"optimizer steps/s ({PRECOND_NAME[args.precond]} + {args.iters} NS iterations)",
+        "value": round(1e3 / ms, 3), "unit": "steps/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(ms, 4), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "f32 parameters, bf16 orthogonalization",
+        "data": "synthetic (seeded power-law gradients, N(0, 0.02^2) parameters)",
+        "config": {"workload": args.workload, "matrices": len(grads), "parameters": n_el,
+                   "shapes": [[c, m, n] for c, m, n, _ in entries], "lr": lr, "momentum": mu,
+                   "nesterov": True},
+        "phase_ms_per_step": phases,
+        "elementwise_gbps": round((14 + 10) * n_el / ((phases["opt_momentum"] + phases["opt_apply"])
+                                                      * 1e-3) / 1e9, 1)
+        if phases["opt_momentum"] + phases["opt_apply"] > 0 else None,
+    }
     print(json.dumps(result), flush=True)
     return 0
 

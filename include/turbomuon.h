@@ -114,6 +114,32 @@ tm_status tm_orthogonalize_grouped_f32(float* const* X, const int64_t* m, const 
                                        int64_t count, int iters, const float* coeffs,
                                        int precond, void* stream);
 
+/*
+ * tm_muon_step_grouped - one optimizer step over `count` fp32 parameter
+ * matrices: Muon's step with its orthogonalization done by this library (the
+ * paper uses Turbo-Muon as a drop-in replacement of Muon's orthogonalization;
+ * its steepest-descent appendix writes the update as -eta PolarFactor(G S)).
+ * Per matrix g (rows m[g], columns n[g], row-major):
+ *
+ *   M <- momentum M + G
+ *   U  = G + momentum M   if nesterov, else U = M      (rounded to bf16)
+ *   O  = the bf16 orthogonalization of U (tm_orthogonalize_grouped semantics:
+ *        iters, coeffs, precond as there)
+ *   W <- W (1 - lr weight_decay) - lr scale O,
+ *        scale = sqrt(max(1, m[g] / n[g])) if shape_scale, else 1
+ *
+ *   W, G, M  host arrays of `count` device pointers to fp32 matrices (4-byte
+ *            aligned; W and M updated in place, G read only; no two of all
+ *            these matrices may overlap).
+ *   m, n     host arrays of sizes, each in 1..TM_MAX_DIM.
+ * U lives in a second library-owned buffer per (device, stream), grown like
+ * the workspace.  Errors as tm_orthogonalize_grouped.
+ */
+tm_status tm_muon_step_grouped(float* const* W, const float* const* G, float* const* M,
+                               const int64_t* m, const int64_t* n, int64_t count, float lr,
+                               float momentum, int nesterov, float weight_decay, int shape_scale,
+                               int iters, const float* coeffs, int precond, void* stream);
+
 /* Bytes of workspace a call with these shapes needs (0 on invalid shapes).
  * dtype_bytes is 2 (bf16) or 4 (fp32). */
 uint64_t tm_workspace_bytes(const int64_t* m, const int64_t* n, int64_t count,
@@ -134,7 +160,9 @@ tm_status tm_release_workspaces(void);
 #define TM_PHASE_COPY_OUT      7  /* iters = 1: result copied into the caller's buffer */
 #define TM_PHASE_LOAD_IN       8  /* bf16: X (or X^T) copied into the zero-padded workspace */
 #define TM_PHASE_SCALE_A       9  /* bf16: A1 = diag(s) A0 diag(s) and X1 = diag(s) X0 */
-#define TM_NUM_PHASES         10
+#define TM_PHASE_OPT_MOMENTUM 10  /* optimizer step: momentum and the bf16 matrix to orthogonalize */
+#define TM_PHASE_OPT_APPLY    11  /* optimizer step: parameter update */
+#define TM_NUM_PHASES         12
 
 /* Timing hooks (a profiling aid for benchmarks).  While enabled, every kernel
  * launch of later calls is bracketed by a pair of HIP events recorded on the

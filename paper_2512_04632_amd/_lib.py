@@ -23,7 +23,8 @@ TM_ERR_HIP = -4
 
 PRECOND = {"none": 0, "frobenius": 1, "frob": 1, "aol": 2, "schatten4": 3, "s4": 3}
 PHASES = {"transpose_in": 0, "frob": 1, "gram": 2, "aol_vector": 3, "poly": 4, "update": 5,
-          "apply_scale": 6, "copy_out": 7, "load_in": 8, "scale_a": 9}
+          "apply_scale": 6, "copy_out": 7, "load_in": 8, "scale_a": 9, "opt_momentum": 10,
+          "opt_apply": 11}
 TM_MAX_DIM = 65536
 TM_MAX_ITERS = 64
 
@@ -43,6 +44,12 @@ _SIGNATURES = {
     "tm_orthogonalize_grouped_f32": (ctypes.c_int, [ctypes.POINTER(ctypes.c_void_p), _c_i64p,
                                                     _c_i64p, ctypes.c_int64, ctypes.c_int, _c_fp,
                                                     ctypes.c_int, ctypes.c_void_p]),
+    "tm_muon_step_grouped": (ctypes.c_int, [ctypes.POINTER(ctypes.c_void_p),
+                                            ctypes.POINTER(ctypes.c_void_p),
+                                            ctypes.POINTER(ctypes.c_void_p), _c_i64p, _c_i64p,
+                                            ctypes.c_int64, ctypes.c_float, ctypes.c_float,
+                                            ctypes.c_int, ctypes.c_float, ctypes.c_int,
+                                            ctypes.c_int, _c_fp, ctypes.c_int, ctypes.c_void_p]),
     "tm_workspace_bytes": (ctypes.c_uint64, [_c_i64p, _c_i64p, ctypes.c_int64, ctypes.c_int]),
     "tm_release_workspaces": (ctypes.c_int, []),
     "tm_timing_enable": (ctypes.c_int, [ctypes.c_int]),
@@ -179,6 +186,44 @@ def orthogonalize_grouped(xs: Sequence, iters: int = 4, coeffs: Optional[Sequenc
                                 ctypes.c_void_p(_stream_handle(xs[0], stream)))
     _check(fn, st)
     return xs
+
+
+def muon_step_grouped(params: Sequence, grads: Sequence, bufs: Sequence, lr: float,
+                      momentum: float = 0.95, nesterov: bool = True, weight_decay: float = 0.0,
+                      shape_scale: bool = True, iters: int = 4, coeffs: Optional[Sequence] = None,
+                      precond="aol", stream=None):
+    """One optimizer step (tm_muon_step_grouped) over lists of 2-D fp32 device tensors.
+
+    params and bufs (momentum buffers) are updated in place; grads are read.
+    """
+    import torch
+    params, grads, bufs = list(params), list(grads), list(bufs)
+    if not (len(params) == len(grads) == len(bufs)):
+        raise ValueError("params, grads and bufs must have the same length")
+    if not params:
+        return
+    dev = params[0].device
+    for w, g, m in zip(params, grads, bufs):
+        for t in (w, g, m):
+            if (not t.is_cuda or t.dtype != torch.float32 or t.dim() != 2 or
+                    not t.is_contiguous() or t.device != dev):
+                raise ValueError("optimizer tensors must be contiguous 2-D fp32 tensors on one device")
+        if g.shape != w.shape or m.shape != w.shape:
+            raise ValueError("gradient and momentum buffer must match the parameter's shape")
+    cnt = len(params)
+    W = (ctypes.c_void_p * cnt)(*[t.data_ptr() for t in params])
+    G = (ctypes.c_void_p * cnt)(*[t.data_ptr() for t in grads])
+    M = (ctypes.c_void_p * cnt)(*[t.data_ptr() for t in bufs])
+    ms = (ctypes.c_int64 * cnt)(*[int(t.shape[0]) for t in params])
+    ns = (ctypes.c_int64 * cnt)(*[int(t.shape[1]) for t in params])
+    carr = _coeff_array(iters, coeffs)
+    with torch.cuda.device(dev):
+        st = lib().tm_muon_step_grouped(W, G, M, ms, ns, cnt, float(lr), float(momentum),
+                                        1 if nesterov else 0, float(weight_decay),
+                                        1 if shape_scale else 0, int(iters), carr,
+                                        _precond(precond),
+                                        ctypes.c_void_p(_stream_handle(params[0], stream)))
+    _check("tm_muon_step_grouped", st)
 
 
 def workspace_bytes(shapes: Sequence, dtype_bytes: int) -> int:

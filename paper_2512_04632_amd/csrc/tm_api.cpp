@@ -4,6 +4,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <cmath>
 #include <array>
 #include <cstdio>
 #include <cstdlib>
@@ -21,6 +22,7 @@ namespace tmk {
 hipError_t launch_elementwise_bf16(int kind, const Phase& P, hipStream_t st);
 hipError_t launch_fast_bf16(int kind, int cfg, const Phase& P, hipStream_t st);
 hipError_t launch_phase_f32(int kind, int cfg, const Phase& P, hipStream_t st);
+hipError_t launch_opt(int apply, const OptPhase& P, hipStream_t st);
 }  // namespace tmk
 
 namespace {
@@ -44,7 +46,9 @@ struct Workspace {
 };
 
 std::mutex g_mu;
-std::map<std::pair<int, hipStream_t>, Workspace> g_ws;
+using WsCache = std::map<std::pair<int, hipStream_t>, Workspace>;
+WsCache g_ws;     // iteration workspace of every call
+WsCache g_ws_u;   // bf16 update matrices of the optimizer step
 std::map<int, bool> g_dev_ok;
 
 // Timing hooks: event pairs bracketing each launch while enabled.
@@ -101,9 +105,9 @@ tm_status check_device(int* dev) {
   return TM_OK;
 }
 
-// Grow the (device, stream) workspace to at least `bytes`.
-tm_status get_workspace(int dev, hipStream_t st, size_t bytes, char** out) {
-  Workspace& w = g_ws[{dev, st}];
+// Grow the (device, stream) buffer of a cache to at least `bytes`.
+tm_status get_workspace(int dev, hipStream_t st, size_t bytes, char** out, WsCache& cache = g_ws) {
+  Workspace& w = cache[{dev, st}];
   if (w.bytes < bytes) {
     if (w.ptr) {
       hipError_t e = hipStreamSynchronize(st);
@@ -401,13 +405,10 @@ tm_status plan_f32(const Plan& pl, int iters, const float* coeffs, int precond) 
   return s;
 }
 
-tm_status run(std::vector<Item>& items, int esz, int iters, const float* coeffs, int precond,
-              hipStream_t st) {
-  if (items.empty()) return TM_OK;
-  std::lock_guard<std::mutex> lock(g_mu);
-  int dev = 0;
-  tm_status s = check_device(&dev);
-  if (s != TM_OK) return s;
+// Plan and enqueue one call (g_mu held, device checked).
+tm_status run_locked(std::vector<Item>& items, int esz, int iters, const float* coeffs,
+                     int precond, hipStream_t st, int dev) {
+  tm_status s = TM_OK;
   int tcfg = 0;
   if (esz == 2) {
     tcfg = choose_tile_cfg(items);
@@ -434,6 +435,48 @@ tm_status run(std::vector<Item>& items, int esz, int iters, const float* coeffs,
   s = get_workspace(dev, st, size_t(total), &pl.ws);
   if (s != TM_OK) return s;
   return esz == 2 ? plan_bf16(pl, iters, coeffs, precond, tcfg) : plan_f32(pl, iters, coeffs, precond);
+}
+
+tm_status run(std::vector<Item>& items, int esz, int iters, const float* coeffs, int precond,
+              hipStream_t st) {
+  if (items.empty()) return TM_OK;
+  std::lock_guard<std::mutex> lock(g_mu);
+  int dev = 0;
+  tm_status s = check_device(&dev);
+  if (s != TM_OK) return s;
+  return run_locked(items, esz, iters, coeffs, precond, st, dev);
+}
+
+// Enqueue one elementwise optimizer launch per chunk of kMaxOptEntries
+// matrices (timed as its own phase when the timing hooks are on).
+tm_status launch_opt(int apply, const std::vector<tmk::OptEntry>& ents, const tmk::OptPhase& base,
+                     hipStream_t st) {
+  for (size_t b0 = 0; b0 < ents.size(); b0 += tmk::kMaxOptEntries) {
+    tmk::OptPhase P = base;
+    const size_t cnt = std::min(ents.size() - b0, size_t(tmk::kMaxOptEntries));
+    uint64_t blocks = 0;
+    for (size_t i = 0; i < cnt; ++i) {
+      P.e[i] = ents[b0 + i];
+      P.e[i].block_start = uint32_t(blocks);
+      blocks += (P.e[i].size + tmk::kOptBlock - 1) / tmk::kOptBlock;
+    }
+    if (blocks >= (uint64_t(1) << 31)) return fail(TM_ERR_UNSUPPORTED, "too many blocks in one launch");
+    P.nent = int32_t(cnt);
+    P.total = uint32_t(blocks);
+    TimedLaunch tl{apply ? int(tmk::kKindOptApply) : int(tmk::kKindOptMomentum), nullptr, nullptr};
+    if (g_timing && P.total > 0) {
+      if (hipEventCreate(&tl.start) != hipSuccess || hipEventCreate(&tl.stop) != hipSuccess)
+        return fail(TM_ERR_HIP, "hipEventCreate failed");
+      (void)hipEventRecord(tl.start, st);
+    }
+    const hipError_t e = tmk::launch_opt(apply, P, st);
+    if (tl.start) {
+      (void)hipEventRecord(tl.stop, st);
+      g_timed.push_back(tl);
+    }
+    if (e != hipSuccess) return fail(TM_ERR_HIP, std::string("kernel launch: ") + hipGetErrorString(e));
+  }
+  return TM_OK;
 }
 
 tm_status check_common(int iters, const float* coeffs, int precond) {
@@ -531,6 +574,66 @@ tm_status tm_orthogonalize_grouped_f32(float* const* X, const int64_t* m, const 
   return grouped(reinterpret_cast<void* const*>(X), m, n, count, iters, coeffs, precond, stream, 4);
 }
 
+tm_status tm_muon_step_grouped(float* const* W, const float* const* G, float* const* M,
+                               const int64_t* m, const int64_t* n, int64_t count, float lr,
+                               float momentum, int nesterov, float weight_decay, int shape_scale,
+                               int iters, const float* coeffs, int precond, void* stream) {
+  g_last_error.clear();
+  tm_status s = check_common(iters, coeffs, precond);
+  if (s != TM_OK) return s;
+  if (count < 0) return fail(TM_ERR_INVALID_ARG, "count < 0");
+  if (count == 0) return TM_OK;
+  if (W == nullptr || G == nullptr || M == nullptr || m == nullptr || n == nullptr)
+    return fail(TM_ERR_INVALID_ARG, "W, G, M, m or n is NULL");
+  for (int64_t g = 0; g < count; ++g) {
+    s = check_shape(m[g], n[g]);
+    if (s != TM_OK) return fail(s, "matrix " + std::to_string(g) + ": " + g_last_error);
+    if (W[g] == nullptr || G[g] == nullptr || M[g] == nullptr)
+      return fail(TM_ERR_INVALID_ARG, "matrix " + std::to_string(g) + ": NULL pointer");
+    if ((reinterpret_cast<uintptr_t>(W[g]) | reinterpret_cast<uintptr_t>(G[g]) |
+         reinterpret_cast<uintptr_t>(M[g])) % 4u != 0)
+      return fail(TM_ERR_UNSUPPORTED, "matrix " + std::to_string(g) + ": pointer not 4-byte aligned");
+  }
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  std::lock_guard<std::mutex> lock(g_mu);
+  int dev = 0;
+  s = check_device(&dev);
+  if (s != TM_OK) return s;
+  uint64_t ubytes = 0;
+  for (int64_t g = 0; g < count; ++g) ubytes += tmk::align256(uint64_t(m[g]) * uint64_t(n[g]) * 2u);
+  char* ubase = nullptr;
+  s = get_workspace(dev, st, size_t(ubytes), &ubase, g_ws_u);
+  if (s != TM_OK) return s;
+  std::vector<tmk::OptEntry> ents(static_cast<size_t>(count));
+  std::vector<Item> items;
+  items.reserve(size_t(count));
+  uint64_t off = 0;
+  for (int64_t g = 0; g < count; ++g) {
+    tmk::OptEntry& E = ents[size_t(g)];
+    std::memset(&E, 0, sizeof(E));
+    E.w = W[g];
+    E.g = G[g];
+    E.m = M[g];
+    E.u = reinterpret_cast<uint16_t*>(ubase + off);
+    E.size = uint64_t(m[g]) * uint64_t(n[g]);
+    E.vec = ((reinterpret_cast<uintptr_t>(W[g]) | reinterpret_cast<uintptr_t>(G[g]) |
+              reinterpret_cast<uintptr_t>(M[g])) & 15u) == 0u;
+    E.scale = shape_scale ? std::sqrt(std::max(1.0f, float(m[g]) / float(n[g]))) : 1.0f;
+    items.push_back(make_item(E.u, m[g], n[g], 1));
+    off += tmk::align256(E.size * 2u);
+  }
+  tmk::OptPhase base;
+  std::memset(&base, 0, sizeof(base));
+  base.lr = lr;
+  base.mu = momentum;
+  base.wd = weight_decay;
+  base.nesterov = nesterov ? 1 : 0;
+  s = launch_opt(0, ents, base, st);                                          // M, bf16 U
+  if (s == TM_OK) s = run_locked(items, 2, iters, coeffs, precond, st, dev);  // U <- O
+  if (s == TM_OK) s = launch_opt(1, ents, base, st);                          // W
+  return s;
+}
+
 uint64_t tm_workspace_bytes(const int64_t* m, const int64_t* n, int64_t count, int dtype_bytes) {
   if (m == nullptr || n == nullptr || count < 0 || (dtype_bytes != 2 && dtype_bytes != 4)) return 0;
   std::vector<Item> items;
@@ -551,11 +654,13 @@ uint64_t tm_workspace_bytes(const int64_t* m, const int64_t* n, int64_t count, i
 
 tm_status tm_release_workspaces(void) {
   std::lock_guard<std::mutex> lock(g_mu);
-  if (g_ws.empty()) return TM_OK;
+  if (g_ws.empty() && g_ws_u.empty()) return TM_OK;
   hipError_t e = hipDeviceSynchronize();
-  for (auto& kv : g_ws)
-    if (kv.second.ptr) (void)hipFree(kv.second.ptr);
-  g_ws.clear();
+  for (WsCache* c : {&g_ws, &g_ws_u}) {
+    for (auto& kv : *c)
+      if (kv.second.ptr) (void)hipFree(kv.second.ptr);
+    c->clear();
+  }
   if (e != hipSuccess) return fail(TM_ERR_HIP, std::string("hipDeviceSynchronize: ") + hipGetErrorString(e));
   return TM_OK;
 }

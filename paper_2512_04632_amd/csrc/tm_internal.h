@@ -81,6 +81,31 @@ struct Phase {
   int32_t tail_base;   // with kTail: first logical tile (of size 2T) covered by the launch
 };
 
+// Optimizer step (fp32 parameters): elementwise launches over the elements of
+// up to kMaxOptEntries matrices, blocks of kOptBlock elements.
+constexpr int kMaxOptEntries = 32;
+constexpr int kOptBlock = 2048;
+
+struct OptEntry {
+  float* w;            // parameter, rows x cols fp32
+  const float* g;      // gradient
+  float* m;            // momentum buffer
+  uint16_t* u;         // bf16 U, then the orthogonalized update O (library workspace)
+  uint64_t size;       // rows * cols
+  uint32_t block_start;  // first block of this matrix in the launch
+  uint32_t vec;        // w, g, m 16-byte aligned: 4-element vectors
+  float scale;         // shape factor of the update
+  uint32_t pad;
+};
+
+struct OptPhase {
+  OptEntry e[kMaxOptEntries];
+  int32_t nent;
+  int32_t nesterov;
+  uint32_t total;      // blocks in the launch (each within one matrix)
+  float lr, mu, wd;
+};
+
 // Tile configurations of the matrix-core kernels (square tiles, 256 threads).
 constexpr int kNumCfg = 3;
 TM_HD int cfg_tile(int cfg) { return cfg == 0 ? 256 : (cfg == 1 ? 128 : 64); }
@@ -88,7 +113,8 @@ TM_HD int cfg_tile(int cfg) { return cfg == 0 ? 256 : (cfg == 1 ? 128 : 64); }
 // Logical blocks per matrix of each kernel.
 // The numbering matches the TM_PHASE_* timing phases of turbomuon.h.
 enum Kind { kKindTransposeIn, kKindFrob, kKindGram, kKindAolVector, kKindPoly,
-            kKindUpdate, kKindApplyScale, kKindCopyOut, kKindLoadIn, kKindScaleA, kNumKinds };
+            kKindUpdate, kKindApplyScale, kKindCopyOut, kKindLoadIn, kKindScaleA,
+            kKindOptMomentum, kKindOptApply, kNumKinds };
 constexpr int kTransposeTile = 64;
 constexpr int kElemBlock = 2048;     // elements per block of the elementwise kernels
 

@@ -124,3 +124,36 @@ def test_workspace_bytes():
     assert tm.workspace_bytes([(4096, 14336)], 2) == layout(4096, 14336, 2)
     assert tm.workspace_bytes([(0, 4)], 2) == 0
     assert tm.workspace_bytes([(4, 4)], 3) == 0
+
+
+def test_muon_step_validation():
+    f = tm.lib().tm_muon_step_grouped
+    P3 = ctypes.c_void_p * 2
+    W, G, M = P3(0x1000, 0x2000), P3(0x3000, 0x4000), P3(0x5000, 0x6000)
+    ms = (ctypes.c_int64 * 2)(8, 16)
+    ns = (ctypes.c_int64 * 2)(8, 4)
+    args = (0.02, 0.95, 1, 0.0, 1, 4, None, 2, None)
+    assert f(W, G, M, ms, ns, 0, *args) == tm.TM_OK                    # empty group: no-op
+    assert f(W, G, M, ms, ns, -1, *args) == tm.TM_ERR_INVALID_ARG
+    assert f(None, G, M, ms, ns, 2, *args) == tm.TM_ERR_INVALID_ARG
+    ns[1] = 0
+    assert f(W, G, M, ms, ns, 2, *args) == tm.TM_ERR_INVALID_ARG
+    assert "matrix 1" in tm.last_error()
+    ns[1] = 4
+    M[1] = None
+    assert f(W, G, M, ms, ns, 2, *args) == tm.TM_ERR_INVALID_ARG
+    M[1] = 0x6002
+    assert f(W, G, M, ms, ns, 2, *args) == tm.TM_ERR_UNSUPPORTED
+    M[1] = 0x6000
+    assert f(W, G, M, ms, ns, 2, 0.02, 0.95, 1, 0.0, 1, 65, None, 2, None) == tm.TM_ERR_INVALID_ARG
+    assert f(W, G, M, ms, ns, 2, 0.02, 0.95, 1, 0.0, 1, 4, None, 7, None) == tm.TM_ERR_INVALID_ARG
+
+
+def test_optimizer_rejects_non_matrix_parameters():
+    torch = pytest.importorskip("torch")
+    from paper_2512_04632_amd.optim import TurboMuon
+    with pytest.raises(ValueError):
+        TurboMuon([torch.nn.Parameter(torch.zeros(5))])
+    with pytest.raises(ValueError):
+        TurboMuon([torch.nn.Parameter(torch.zeros(4, 4, dtype=torch.float64))])
+    TurboMuon([torch.nn.Parameter(torch.zeros(4, 6))], lr=0.1)
