@@ -147,23 +147,29 @@ int choose_cfg(int kind, const std::vector<Item>& items) {
   return tmk::kNumCfg - 1;
 }
 
-// bf16 path: one square tile for every phase of the call.  Take the largest
-// tile whose zero padding adds at most 30% to the call's products and whose
-// update still has about two waves of tiles for the 256 compute units.
+// bf16 path: the layout tile of the call (the Gram and polynomial may run
+// smaller tiles of it).  Take the largest tile whose zero padding adds at most
+// 30% to the call's products and whose update still has about two waves of
+// tiles for the 256 compute units; the 256 tile also needs update tiles with
+// a mean K of at least 512, below which its fixed costs per tile (pipeline
+// fill, the 128 KB epilogue) outweigh its faster main loop.
 int choose_tile_cfg(const std::vector<Item>& items) {
   double real = 0.0;
   for (const Item& it : items)
     real += double(it.count) * (3.0 * it.k * double(it.k) * it.N + double(it.k) * it.k * it.k);
   for (int cfg = 0; cfg < tmk::kNumCfg - 1; ++cfg) {
     const uint32_t T = uint32_t(tmk::cfg_tile(cfg));
-    double padded = 0.0, tiles = 0.0;
+    double padded = 0.0, tiles = 0.0, ksum = 0.0;
     for (const Item& it : items) {
       uint32_t kp, Np;
       tmk::tiled_dims(it.k, it.N, T, &kp, &Np);
       padded += double(it.count) * (3.0 * kp * double(kp) * Np + double(kp) * kp * kp);
-      tiles += double(it.count) * (kp / T) * (Np / T);
+      const double t = double(it.count) * (kp / T) * (Np / T);
+      tiles += t;
+      ksum += t * kp;
     }
-    if (padded <= 1.3 * real && tiles >= 480.0) return cfg;
+    const bool long_k = T < 256 || ksum >= 512.0 * tiles;
+    if (padded <= 1.3 * real && tiles >= 480.0 && long_k) return cfg;
   }
   return tmk::kNumCfg - 1;
 }
