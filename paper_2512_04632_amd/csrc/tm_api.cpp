@@ -20,7 +20,7 @@
 
 namespace tmk {
 hipError_t launch_elementwise_bf16(int kind, const Phase& P, hipStream_t st);
-hipError_t launch_fast_bf16(int kind, int cfg, const Phase& P, hipStream_t st);
+hipError_t launch_fast_bf16(int kind, int cfg, bool wide, const Phase& P, hipStream_t st);
 hipError_t launch_phase_f32(int kind, int cfg, const Phase& P, hipStream_t st);
 hipError_t launch_opt(int apply, const OptPhase& P, hipStream_t st);
 }  // namespace tmk
@@ -201,6 +201,24 @@ struct Plan {
 // Compute units of the MI355X: the blocks of one full wave of the large tiles.
 constexpr int kWave = 256;
 
+// The wide K step of a bf16 matrix-core launch: only for launches of at most
+// one wave of blocks (its larger ring holds one workgroup per compute unit,
+// which a launch with more blocks than units would feel), and only when every
+// K of the launch is a multiple of the step: the Gram contracts over Np, the
+// polynomial and the update over kp.
+bool wide_step_ok(int kind, int cfg, const Phase& P) {
+#ifdef TM_NO_WIDE_K_STEP
+  return false;
+#endif
+  const uint32_t step = uint32_t(tmk::wide_k_step(tmk::cfg_tile(cfg)));
+  if (step == 32u || P.total > kWave) return false;
+  for (int e = 0; e < P.nent; ++e) {
+    const uint32_t K = kind == tmk::kKindGram ? P.e[e].Np : P.e[e].kp;
+    if (P.e[e].tiles_per != 0u && K % step != 0u) return false;
+  }
+  return true;
+}
+
 // Enqueue one kernel launch of a prepared phase descriptor (timed when the
 // timing hooks are on).
 tm_status fire(const Plan& pl, int kind, int cfg, const Phase& P) {
@@ -216,7 +234,7 @@ tm_status fire(const Plan& pl, int kind, int cfg, const Phase& P) {
   else if (kind == tmk::kKindFrob || kind == tmk::kKindAolVector || kind == tmk::kKindApplyScale)
     e = tmk::launch_elementwise_bf16(kind, P, pl.st);
   else
-    e = tmk::launch_fast_bf16(kind, cfg, P, pl.st);
+    e = tmk::launch_fast_bf16(kind, cfg, wide_step_ok(kind, cfg, P), P, pl.st);
   if (tl.start) {
     (void)hipEventRecord(tl.stop, pl.st);
     g_timed.push_back(tl);

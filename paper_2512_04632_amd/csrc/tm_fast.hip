@@ -42,12 +42,6 @@ typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x16_t __attribute__((ext_vector_type(16)));
 typedef short s16x4_t __attribute__((ext_vector_type(4)));
 
-#ifndef TM_FAST_STAGES
-#define TM_FAST_STAGES 4
-#endif
-constexpr int BK = 32;        // K elements per stage (64 bytes of a K-contiguous row)
-constexpr int STAGES = TM_FAST_STAGES;
-
 // Tile T x T computed by NW wave64s in a 2 x (NW/2) grid; each wave owns
 // (T/2) x (2T/NW) of the output as 32 x 32 MFMA blocks.
 template <int T>
@@ -56,11 +50,25 @@ struct Tile {
   static constexpr int NT = 64 * NW;            // threads per workgroup
   static constexpr int TWM = T / 2, TWN = 2 * T / NW;
   static constexpr int FM = TWM / 32, FN = TWN / 32;
-  static constexpr int A_BYTES = T * BK * 2;    // one operand stage
+};
+
+// LDS ring of one main loop: NSTAGE stages of BK K-elements of both operands.
+// A K-contiguous operand row of a stage is RB = 2 BK bytes, stored as CPR
+// 16-byte chunks; logical chunk c of row r lives at chunk c ^ ((r / RPB) %
+// CPR), RPB being the rows that span the 64 banks once, so that the 16 lanes
+// of a ds_read_b128 pass (16 rows, one chunk) hit every bank once.
+template <int T, int BK>
+struct Ring {
+  static constexpr int NSTAGE = BK == 32 ? 4 : 3;
+  static constexpr int RB = 2 * BK;
+  static constexpr int CPR = RB / 16;
+  static constexpr int RPB = 256 / RB;
+  static constexpr int A_BYTES = T * RB;         // one operand stage
   static constexpr int STAGE = 2 * A_BYTES;
-  static constexpr int LDS = STAGES * STAGE;
-  static constexpr int DMA_OP = T / 16 / NW;    // DMA instructions per wave per operand per stage
+  static constexpr int LDS = NSTAGE * STAGE;
+  static constexpr int DMA_OP = T * BK / 512 / Tile<T>::NW;   // 1 KB DMAs per wave per operand
   static constexpr int PER_STAGE = 2 * DMA_OP;
+  static_assert(T * BK % (512 * Tile<T>::NW) == 0, "whole DMA instructions per wave");
   static_assert(LDS <= 160 * 1024, "gfx950 LDS is 160 KB per workgroup");
 };
 
@@ -103,6 +111,7 @@ __device__ inline void ring_sync_dma() {
   else if constexpr (PENDING == 12) asm volatile("s_waitcnt vmcnt(12)\n\ts_barrier" ::: "memory");
   else if constexpr (PENDING == 16) asm volatile("s_waitcnt vmcnt(16)\n\ts_barrier" ::: "memory");
   else if constexpr (PENDING == 24) asm volatile("s_waitcnt vmcnt(24)\n\ts_barrier" ::: "memory");
+  else if constexpr (PENDING == 32) asm volatile("s_waitcnt vmcnt(32)\n\ts_barrier" ::: "memory");
   else static_assert(PENDING == 0, "unsupported in-flight count");
 }
 
@@ -149,16 +158,19 @@ __device__ inline void barrier_pinned() {
 }
 
 // ---------------------------------------------------------------- DMA issue
-// K-contiguous operand: T rows x 32 bf16 (64 bytes).  Logical 16-byte chunk c
-// of row r lives at chunk c ^ ((r >> 2) & 3).  One instruction fills 16 rows.
-template <int T>
+// K-contiguous operand: T rows x BK bf16 in the swizzled row layout of Ring.
+// One instruction fills 1 KB = 64 / CPR rows; lane i writes chunk i % CPR of
+// its row, i.e. it loads logical chunk (i % CPR) ^ swizzle.
+template <int T, int BK>
 __device__ inline void issue_kc(const uint16_t* src, int64_t ld, int k0, uint32_t lds) {
+  using R = Ring<T, BK>;
+  constexpr int RPI = 64 / R::CPR;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
 #pragma unroll
-  for (int q = 0; q < Tile<T>::DMA_OP; ++q) {
+  for (int q = 0; q < R::DMA_OP; ++q) {
     const int j = wave + Tile<T>::NW * q;
-    const int r = j * 16 + (lane >> 2);
-    const int c = (lane & 3) ^ ((r >> 2) & 3);
+    const int r = j * RPI + lane / R::CPR;
+    const int c = (lane % R::CPR) ^ ((r / R::RPB) % R::CPR);
     const uint32_t voff = uint32_t((int64_t(r) * ld + k0 + c * 8) * 2);
     dma16(src, voff, __builtin_amdgcn_readfirstlane(lds + uint32_t(j) * 1024u));
   }
@@ -170,15 +182,15 @@ __device__ inline int swz_y(int r) {
   return T >= 128 ? 2 * (r & 3) : 2 * ((r >> 1) & 1);
 }
 
-// Row-major operand (the update's Y): 32 rows (K) x T columns, row = 2T bytes.
-template <int T>
+// Row-major operand (the update's Y): BK rows (K) x T columns, row = 2T bytes.
+template <int T, int BK>
 __device__ inline void issue_rm(const uint16_t* src, int64_t ld, int k0, uint32_t lds) {
   constexpr int ROWB = 2 * T;
   constexpr int LPR = ROWB / 16;          // lanes per row
   constexpr int RPI = 1024 / ROWB;        // rows per instruction
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
 #pragma unroll
-  for (int q = 0; q < Tile<T>::DMA_OP; ++q) {
+  for (int q = 0; q < Ring<T, BK>::DMA_OP; ++q) {
     const int j = wave + Tile<T>::NW * q;
     const int r = j * RPI + lane / LPR;
     const int p16 = lane % LPR;
@@ -195,23 +207,24 @@ struct Frags {
 };
 
 // MFMA operands of K slice kk (16 wide) of one stage.
-template <int T, bool RM>
+template <int T, bool RM, int BK>
 __device__ inline void load_frags(Frags<T>& fr, const char* sa, const char* sb, int kk, int wm,
                                   int wn) {
   constexpr int FM = Tile<T>::FM, FN = Tile<T>::FN;
+  using R = Ring<T, BK>;
   const int lane = threadIdx.x & 63;
   const int lr = lane & 31, lh = lane >> 5;
   const int c = 2 * kk + lh;
 #pragma unroll
   for (int f = 0; f < FM; ++f) {
     const int r = wm * Tile<T>::TWM + f * 32 + lr;
-    fr.a[f] = *reinterpret_cast<const uint4*>(sa + r * 64 + 16 * (c ^ ((r >> 2) & 3)));
+    fr.a[f] = *reinterpret_cast<const uint4*>(sa + r * R::RB + 16 * (c ^ ((r / R::RPB) % R::CPR)));
   }
   if constexpr (!RM) {
 #pragma unroll
     for (int f = 0; f < FN; ++f) {
       const int r = wn * Tile<T>::TWN + f * 32 + lr;
-      fr.b[f] = *reinterpret_cast<const uint4*>(sb + r * 64 + 16 * (c ^ ((r >> 2) & 3)));
+      fr.b[f] = *reinterpret_cast<const uint4*>(sb + r * R::RB + 16 * (c ^ ((r / R::RPB) % R::CPR)));
     }
   } else {
     // Lane q of 16-lane group g addresses row kb + q/4, columns n + 4(q%4);
@@ -259,16 +272,20 @@ __device__ inline void mma(f32x16_t (&acc)[Tile<T>::FM][Tile<T>::FN], const Frag
 // K-contiguous rows of b (RM = false) or B = the K x T row-major block of b
 // (RM = true).  K is a multiple of BK; every tile is full.
 //
-// Schedule per stage kt (two K slices of 16): the operands of slice 0 were
-// read before the stage began; slice 1 is read while slice 0's MFMAs run;
-// then the ring is synchronised for stage kt+1 (its DMA done in every wave,
-// and every wave done reading stage kt), the DMA of stage kt+4 reuses stage
-// kt's buffer, and slice 0 of stage kt+1 is read while slice 1's MFMAs run.
-template <int T, bool RM, bool SWAP = false>
+// Schedule per stage kt (BK / 16 K slices of 16): the operands of slice 0
+// were read before the stage began; every slice's operands are read while
+// the previous slice's MFMAs run; before the last slice's MFMAs the ring is
+// synchronised for stage kt+1 (its DMA done in every wave, and every wave
+// done reading stage kt), the DMA of stage kt + NSTAGE reuses stage kt's
+// buffer, and slice 0 of stage kt+1 is read while the last slice's MFMAs run.
+// The K slices are consumed in increasing order whatever BK is, so every
+// output element accumulates the same products in the same order.
+template <int T, bool RM, bool SWAP, int BK>
 __device__ inline void mainloop(f32x16_t (&acc)[Tile<T>::FM][Tile<T>::FN], char* smem,
                                 const uint16_t* a, int64_t lda, const uint16_t* b, int64_t ldb,
                                 int K) {
-  constexpr int PS = Tile<T>::PER_STAGE;
+  using R = Ring<T, BK>;
+  constexpr int PS = R::PER_STAGE, NS = BK / 16, NST = R::NSTAGE;
   const int wave = threadIdx.x >> 6;
   const int wm = wave / (Tile<T>::NW / 2), wn = wave % (Tile<T>::NW / 2);
 #pragma unroll
@@ -281,36 +298,40 @@ __device__ inline void mainloop(f32x16_t (&acc)[Tile<T>::FM][Tile<T>::FN], char*
   const uint32_t lds0 = lds_addr(smem);
   const int nk = K / BK;
   auto issue = [&](int kt) {
-    const uint32_t st = lds0 + uint32_t((kt % STAGES) * Tile<T>::STAGE);
-    issue_kc<T>(a, lda, kt * BK, st);
-    if constexpr (RM) issue_rm<T>(b, ldb, kt * BK, st + Tile<T>::A_BYTES);
-    else issue_kc<T>(b, ldb, kt * BK, st + Tile<T>::A_BYTES);
+    const uint32_t st = lds0 + uint32_t((kt % NST) * R::STAGE);
+    issue_kc<T, BK>(a, lda, kt * BK, st);
+    if constexpr (RM) issue_rm<T, BK>(b, ldb, kt * BK, st + R::A_BYTES);
+    else issue_kc<T, BK>(b, ldb, kt * BK, st + R::A_BYTES);
   };
-  auto stage_ptr = [&](int kt) { return smem + (kt % STAGES) * Tile<T>::STAGE; };
+  auto stage_ptr = [&](int kt) { return smem + (kt % NST) * R::STAGE; };
 #pragma unroll
-  for (int s = 0; s < STAGES; ++s)
+  for (int s = 0; s < NST; ++s)
     if (s < nk) issue(s);
-  ring_wait<PS>(min(nk - 1, STAGES - 1));
+  ring_wait<PS>(min(nk - 1, NST - 1));
 
   Frags<T> f0, f1;
-  load_frags<T, RM>(f0, stage_ptr(0), stage_ptr(0) + Tile<T>::A_BYTES, 0, wm, wn);
-  for (int kt = 0; kt + 1 < nk; ++kt) {
+  load_frags<T, RM, BK>(f0, stage_ptr(0), stage_ptr(0) + R::A_BYTES, 0, wm, wn);
+  for (int kt = 0; kt < nk; ++kt) {
     const char* st = stage_ptr(kt);
-    load_frags<T, RM>(f1, st, st + Tile<T>::A_BYTES, 1, wm, wn);
-    mma<T, SWAP>(acc, f0);
-    __builtin_amdgcn_sched_barrier(0);
-    ring_wait<PS>(min(nk - 1, kt + STAGES - 1) - (kt + 1));
-    if (kt + STAGES < nk) issue(kt + STAGES);
-    const char* nx = stage_ptr(kt + 1);
-    load_frags<T, RM>(f0, nx, nx + Tile<T>::A_BYTES, 0, wm, wn);
-    __builtin_amdgcn_sched_barrier(0);
-    mma<T, SWAP>(acc, f1);
-  }
-  {
-    const char* st = stage_ptr(nk - 1);
-    load_frags<T, RM>(f1, st, st + Tile<T>::A_BYTES, 1, wm, wn);
-    mma<T, SWAP>(acc, f0);
-    mma<T, SWAP>(acc, f1);
+#pragma unroll
+    for (int s = 0; s < NS; s += 2) {
+      load_frags<T, RM, BK>(f1, st, st + R::A_BYTES, s + 1, wm, wn);
+      mma<T, SWAP>(acc, f0);
+      if (s + 2 < NS) {
+        load_frags<T, RM, BK>(f0, st, st + R::A_BYTES, s + 2, wm, wn);
+        mma<T, SWAP>(acc, f1);
+      } else {
+        __builtin_amdgcn_sched_barrier(0);
+        if (kt + 1 < nk) {
+          ring_wait<PS>(min(nk - 1, kt + NST - 1) - (kt + 1));
+          if (kt + NST < nk) issue(kt + NST);
+          const char* nx = stage_ptr(kt + 1);
+          load_frags<T, RM, BK>(f0, nx, nx + R::A_BYTES, 0, wm, wn);
+        }
+        __builtin_amdgcn_sched_barrier(0);
+        mma<T, SWAP>(acc, f1);
+      }
+    }
   }
   ring_sync<0>();   // the ring is free for the epilogue
 }
@@ -333,7 +354,10 @@ __device__ inline void mainloop_pp(f32x16_t (&acc)[Tile<T>::FM][Tile<T>::FN], ch
                                    const uint16_t* a, int64_t lda, const uint16_t* b,
                                    int64_t ldb, int K) {
   static_assert(Tile<T>::NW == 8, "ping-pong needs two waves per SIMD");
-  constexpr int PS = Tile<T>::PER_STAGE;
+  constexpr int BK = 32, STAGES = 4;
+  using R = Ring<T, BK>;
+  static_assert(R::NSTAGE == STAGES, "ring depth");
+  constexpr int PS = R::PER_STAGE;
   const int wave = threadIdx.x >> 6;
   const int wm = wave / 4, wn = wave % 4;
   const bool g1 = __builtin_amdgcn_readfirstlane(wave) >= 4;
@@ -347,12 +371,12 @@ __device__ inline void mainloop_pp(f32x16_t (&acc)[Tile<T>::FM][Tile<T>::FN], ch
   const uint32_t lds0 = lds_addr(smem);
   const int nk = K / BK;
   auto issue = [&](int kt) {
-    const uint32_t st = lds0 + uint32_t((kt % STAGES) * Tile<T>::STAGE);
-    issue_kc<T>(a, lda, kt * BK, st);
-    if constexpr (RM) issue_rm<T>(b, ldb, kt * BK, st + Tile<T>::A_BYTES);
-    else issue_kc<T>(b, ldb, kt * BK, st + Tile<T>::A_BYTES);
+    const uint32_t st = lds0 + uint32_t((kt % STAGES) * R::STAGE);
+    issue_kc<T, BK>(a, lda, kt * BK, st);
+    if constexpr (RM) issue_rm<T, BK>(b, ldb, kt * BK, st + R::A_BYTES);
+    else issue_kc<T, BK>(b, ldb, kt * BK, st + R::A_BYTES);
   };
-  auto stage_ptr = [&](int kt) { return smem + (kt % STAGES) * Tile<T>::STAGE; };
+  auto stage_ptr = [&](int kt) { return smem + (kt % STAGES) * R::STAGE; };
 #pragma unroll
   for (int s = 0; s + 1 < STAGES; ++s)
     if (s < nk) issue(s);
@@ -364,8 +388,8 @@ __device__ inline void mainloop_pp(f32x16_t (&acc)[Tile<T>::FM][Tile<T>::FN], ch
     // MEM(j)
     if (j + STAGES - 1 < nk) issue(j + STAGES - 1);
     const char* st = stage_ptr(j);
-    load_frags<T, RM>(f0, st, st + Tile<T>::A_BYTES, 0, wm, wn);
-    load_frags<T, RM>(f1, st, st + Tile<T>::A_BYTES, 1, wm, wn);
+    load_frags<T, RM, BK>(f0, st, st + R::A_BYTES, 0, wm, wn);
+    load_frags<T, RM, BK>(f1, st, st + R::A_BYTES, 1, wm, wn);
     const int pend = min(nk - 1, j + STAGES - 1) - (j + 1);
     if (g1) {
       __builtin_amdgcn_s_waitcnt(0xC07F);   // lgkmcnt(0)
@@ -383,17 +407,16 @@ __device__ inline void mainloop_pp(f32x16_t (&acc)[Tile<T>::FM][Tile<T>::FN], ch
   dma_wait<0>();   // nothing is in flight here; keeps the counter model exact
 }
 
-template <int T, bool RM, bool SWAP = false>
+template <int T, bool RM, bool SWAP, int BK>
 __device__ inline void run_mainloop(f32x16_t (&acc)[Tile<T>::FM][Tile<T>::FN], char* smem,
                                     const uint16_t* a, int64_t lda, const uint16_t* b,
                                     int64_t ldb, int K) {
-#ifndef TM_NO_PINGPONG
   if constexpr (Tile<T>::NW == 8) {
+    static_assert(BK == 32, "the 8-wave tile runs 32-wide K steps");
     mainloop_pp<T, RM, SWAP>(acc, smem, a, lda, b, ldb, K);
-    return;
+  } else {
+    mainloop<T, RM, SWAP, BK>(acc, smem, a, lda, b, ldb, K);
   }
-#endif
-  mainloop<T, RM, SWAP>(acc, smem, a, lda, b, ldb, K);
 }
 
 // ---------------------------------------------------------------- mapping
@@ -507,9 +530,9 @@ struct Stage {
   static constexpr int PER_THREAD = T * CPR / Tile<T>::NT;  // chunks per thread
 };
 
-template <int T>
+template <int T, int BK>
 constexpr int smem_bytes() {
-  return Tile<T>::LDS > Stage<T>::BYTES ? Tile<T>::LDS : Stage<T>::BYTES;
+  return Ring<T, BK>::LDS > Stage<T>::BYTES ? Ring<T, BK>::LDS : Stage<T>::BYTES;
 }
 
 // LDS row r of the stage -> dst row row0 + r, columns col0.. (whole tile).
@@ -670,9 +693,9 @@ __device__ inline void store_sym_f32(const f32x16_t (&acc)[Tile<T>::FM][Tile<T>:
 }
 
 // ---------------------------------------------------------------- kernels
-template <int T>
+template <int T, int BK>
 __global__ __launch_bounds__(Tile<T>::NT) void k_gram_fast(const Phase P) {
-  __shared__ __attribute__((aligned(1024))) char smem[smem_bytes<T>()];
+  __shared__ __attribute__((aligned(1024))) char smem[smem_bytes<T, BK>()];
   constexpr int FM = Tile<T>::FM, FN = Tile<T>::FN;
   Loc L;
   int I, J;
@@ -684,7 +707,7 @@ __global__ __launch_bounds__(Tile<T>::NT) void k_gram_fast(const Phase P) {
   const WsLayout WL = ws_layout(E.kp, E.Np, 2);
   const int64_t ldy = WL.ldy;
   f32x16_t acc[FM][FN];
-  run_mainloop<T, false>(acc, smem, Y + int64_t(I) * T * ldy, ldy, Y + int64_t(J) * T * ldy, ldy, Np);
+  run_mainloop<T, false, false, BK>(acc, smem, Y + int64_t(I) * T * ldy, ldy, Y + int64_t(J) * T * ldy, ldy, Np);
 
   if (P.flags & kA32) {
     store_sym_f32<T>(acc, reinterpret_cast<float*>(w + WL.a32), kp, I, J);
@@ -750,9 +773,9 @@ __global__ __launch_bounds__(Tile<T>::NT) void k_gram_fast(const Phase P) {
 
 // B~ = b A + c A A + a I (upper tiles, mirrored).  The stage is preloaded with
 // A's tile (J, I), whose element (j, i) equals A_ij.
-template <int T>
+template <int T, int BK>
 __global__ __launch_bounds__(Tile<T>::NT) void k_poly_fast(const Phase P) {
-  __shared__ __attribute__((aligned(1024))) char smem[smem_bytes<T>()];
+  __shared__ __attribute__((aligned(1024))) char smem[smem_bytes<T, BK>()];
   constexpr int FM = Tile<T>::FM, FN = Tile<T>::FN;
   Loc L;
   int I, J;
@@ -765,7 +788,7 @@ __global__ __launch_bounds__(Tile<T>::NT) void k_poly_fast(const Phase P) {
   uint16_t* B = reinterpret_cast<uint16_t*>(w + WL.b);
   const int64_t ldg = WL.ldg;
   f32x16_t acc[FM][FN];
-  run_mainloop<T, false>(acc, smem, A + int64_t(I) * T * ldg, ldg, A + int64_t(J) * T * ldg, ldg, kp);
+  run_mainloop<T, false, false, BK>(acc, smem, A + int64_t(I) * T * ldg, ldg, A + int64_t(J) * T * ldg, ldg, kp);
   load_rows<T>(smem, A, ldg, int64_t(J) * T, int64_t(I) * T);
   __syncthreads();
   const float a = P.a, b = P.b, c = P.c;
@@ -780,9 +803,9 @@ __global__ __launch_bounds__(Tile<T>::NT) void k_poly_fast(const Phase P) {
 // consecutive columns of an output row; the tile goes out through the stage.
 // dst = kSlotFinal writes the caller's matrix (tall: transposed), otherwise
 // the workspace slot.
-template <int T>
+template <int T, int BK>
 __global__ __launch_bounds__(Tile<T>::NT) void k_update_fast(const Phase P) {
-  __shared__ __attribute__((aligned(1024))) char smem[smem_bytes<T>()];
+  __shared__ __attribute__((aligned(1024))) char smem[smem_bytes<T, BK>()];
   constexpr int FM = Tile<T>::FM, FN = Tile<T>::FN;
   // Logical tile -> (block row, block column) in groups of 4 block rows, so
   // that concurrently running tiles share rows of B~.  Under kTail the launch
@@ -810,7 +833,7 @@ __global__ __launch_bounds__(Tile<T>::NT) void k_update_fast(const Phase P) {
   const uint16_t* Y = wbuf(P, E, L.mat, P.src);
   const int64_t ldg = WL.ldg, ldy = WL.ldy;
   f32x16_t acc[FM][FN];
-  run_mainloop<T, true, true>(acc, smem, B + int64_t(I) * T * ldg, ldg, Y + int64_t(Lb) * T, ldy, kp);
+  run_mainloop<T, true, true, BK>(acc, smem, B + int64_t(I) * T * ldg, ldg, Y + int64_t(Lb) * T, ldy, kp);
 
   // acc[fm][fn] element v: output row i = wm*TWM + fm*32 + lane%32, columns
   // l0..l0+3 with l0 = wn*TWN + fn*32 + 8(v/4) + 4(lane/32)
@@ -923,19 +946,19 @@ __global__ __launch_bounds__(256) void k_apply_s(const Phase P) {
 #define TM_LAUNCH(kern) \
   do { hipLaunchKernelGGL(kern, dim3(P.total), dim3(Tile<T>::NT), 0, st, P); return hipGetLastError(); } while (0)
 
-template <int T>
+template <int T, int BK>
 static hipError_t launch_t(int kind, const Phase& P, hipStream_t st) {
   switch (kind) {
-    case kKindGram: TM_LAUNCH(k_gram_fast<T>);
-    case kKindPoly: TM_LAUNCH(k_poly_fast<T>);
-    case kKindUpdate: TM_LAUNCH(k_update_fast<T>);
+    case kKindGram: TM_LAUNCH((k_gram_fast<T, BK>));
+    case kKindPoly: TM_LAUNCH((k_poly_fast<T, BK>));
+    case kKindUpdate: TM_LAUNCH((k_update_fast<T, BK>));
   }
   return hipErrorInvalidValue;
 }
 
 }  // namespace fast
 
-hipError_t launch_fast_bf16(int kind, int cfg, const Phase& P, hipStream_t st) {
+hipError_t launch_fast_bf16(int kind, int cfg, bool wide, const Phase& P, hipStream_t st) {
   if (P.total <= 0) return hipSuccess;
   if (kind == kKindLoadIn) {
     hipLaunchKernelGGL(fast::k_load_in, dim3(P.total), dim3(256), 0, st, P);
@@ -946,9 +969,13 @@ hipError_t launch_fast_bf16(int kind, int cfg, const Phase& P, hipStream_t st) {
     return hipGetLastError();
   }
   switch (cfg_tile(cfg)) {
-    case 256: return fast::launch_t<256>(kind, P, st);
-    case 128: return fast::launch_t<128>(kind, P, st);
-    case 64: return fast::launch_t<64>(kind, P, st);
+    case 256: return fast::launch_t<256, 32>(kind, P, st);
+    case 128:
+      return wide ? fast::launch_t<128, wide_k_step(128)>(kind, P, st)
+                  : fast::launch_t<128, 32>(kind, P, st);
+    case 64:
+      return wide ? fast::launch_t<64, wide_k_step(64)>(kind, P, st)
+                  : fast::launch_t<64, 32>(kind, P, st);
   }
   return hipErrorInvalidValue;
 }
