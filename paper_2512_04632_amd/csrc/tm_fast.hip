@@ -158,6 +158,10 @@ __device__ inline void barrier_pinned() {
 }
 
 // ---------------------------------------------------------------- DMA issue
+// The per-lane offset of a DMA is 32 bits: the base address of every call
+// starts at the tile's first row (kc) or the stage's first row (rm), so an
+// offset spans at most 256 rows of a row of at most 65536 + 7 elements.
+//
 // K-contiguous operand: T rows x BK bf16 in the swizzled row layout of Ring.
 // One instruction fills 1 KB = 64 / CPR rows; lane i writes chunk i % CPR of
 // its row, i.e. it loads logical chunk (i % CPR) ^ swizzle.
@@ -183,20 +187,23 @@ __device__ inline int swz_y(int r) {
 }
 
 // Row-major operand (the update's Y): BK rows (K) x T columns, row = 2T bytes.
+// The stage's first row goes into the 64-bit base address, so the 32-bit
+// per-lane offset spans BK rows only, whatever the matrix size.
 template <int T, int BK>
 __device__ inline void issue_rm(const uint16_t* src, int64_t ld, int k0, uint32_t lds) {
   constexpr int ROWB = 2 * T;
   constexpr int LPR = ROWB / 16;          // lanes per row
   constexpr int RPI = 1024 / ROWB;        // rows per instruction
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const uint16_t* base = src + int64_t(k0) * ld;
 #pragma unroll
   for (int q = 0; q < Ring<T, BK>::DMA_OP; ++q) {
     const int j = wave + Tile<T>::NW * q;
     const int r = j * RPI + lane / LPR;
     const int p16 = lane % LPR;
     const int c = (p16 >> 1) ^ swz_y<T>(r);
-    const uint32_t voff = uint32_t((int64_t(k0 + r) * ld + c * 16 + (p16 & 1) * 8) * 2);
-    dma16(src, voff, __builtin_amdgcn_readfirstlane(lds + uint32_t(j) * 1024u));
+    const uint32_t voff = uint32_t((int64_t(r) * ld + c * 16 + (p16 & 1) * 8) * 2);
+    dma16(base, voff, __builtin_amdgcn_readfirstlane(lds + uint32_t(j) * 1024u));
   }
 }
 

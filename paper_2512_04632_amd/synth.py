@@ -87,6 +87,46 @@ def cast(x: np.ndarray, dtype: str) -> np.ndarray:
     raise ValueError(f"unknown dtype {dtype!r}")
 
 
+def block_diagonal_layout(m: int, n: int, count: int):
+    """Split an m x n matrix into `count` blocks along its diagonal.
+
+    Rows and columns are each cut into `count` runs whose lengths differ by at
+    most one (the longer runs first); block i covers rows [r0, r1) and columns
+    [c0, c1) of run i.  Returns a list of (r0, r1, c0, c1).  Every block has
+    the orientation of the whole matrix (no taller than wide when m <= n, taller
+    than wide otherwise), so a per-block computation that picks its side from
+    the shape picks the same side as the whole.
+    """
+    if not (1 <= count <= min(m, n)):
+        raise ValueError("count must be in 1..min(m, n)")
+
+    def runs(total):
+        q, r = divmod(total, count)
+        edges = [0]
+        for i in range(count):
+            edges.append(edges[-1] + q + (1 if i < r else 0))
+        return edges
+
+    re, ce = runs(m), runs(n)
+    out = [(re[i], re[i + 1], ce[i], ce[i + 1]) for i in range(count)]
+    for r0, r1, c0, c1 in out:
+        if (m <= n) != (r1 - r0 <= c1 - c0):
+            raise ValueError(f"block {r1 - r0} x {c1 - c0} is not oriented as {m} x {n}")
+    return out
+
+
+def block_diagonal_blocks(m: int, n: int, count: int, alpha: float, seed: int):
+    """Layout and float64 contents of a block-diagonal m x n input.
+
+    Block i is ``power_law_matrix`` of its shape with seed ``seed + i``; every
+    entry outside the blocks is zero.
+    """
+    layout = block_diagonal_layout(m, n, count)
+    blocks = [power_law_matrix(r1 - r0, c1 - c0, alpha, seed + i)
+              for i, (r0, r1, c0, c1) in enumerate(layout)]
+    return layout, blocks
+
+
 # Workloads: (count, m, n, alpha).  Matrix i of a workload, counted across
 # its entries in the listed order, uses seed = base + i.
 WORKLOADS = {

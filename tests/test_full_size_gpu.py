@@ -7,6 +7,10 @@ of the same shape runs them on 128 x 128 tiles throughout.  Every output
 element accumulates the same products in the same order either way, so a
 matrix must come out of the batched call bit for bit as from its own call.
 Matrix 0 of the 8 x 4096 x 14336 batch is checked against the fp64 oracle.
+
+At the maximum sizes (one side 65536) the oracle cannot run on the whole
+matrix; a block-diagonal input stays block-diagonal through AOL and every
+iteration, so each block is checked against the oracle on that block.
 """
 import numpy as np
 import pytest
@@ -43,6 +47,46 @@ def test_llm8b_4096x14336_batch_of_8():
     log(f"matrix 0: relF={e:.3e} eps_ortho ratio={r:.4f}")
     assert e <= BF16_TOL and abs(r - 1) <= EO_RATIO_TOL
     assert torch.isfinite(B.float()).all()
+
+
+def _block_diagonal_case(m, n, count, seed):
+    """Block-diagonal m x n bf16 input: each block against the oracle's output
+    for that block alone, and every entry outside the blocks exactly zero
+    (zeros multiply and add to exact zeros in every phase)."""
+    layout, blocks = synth.block_diagonal_blocks(m, n, count, 0.8, seed)
+    blocks = [synth.cast(b, "bf16") for b in blocks]
+    X = torch.zeros((m, n), dtype=torch.bfloat16, device="cuda")
+    for (r0, r1, c0, c1), b in zip(layout, blocks):
+        X[r0:r1, c0:c1] = torch.from_numpy(b.astype(np.float32)).to(torch.bfloat16).cuda()
+    tm.orthogonalize(X, 4, None, "aol")
+    torch.cuda.synchronize()
+    worst = 0.0
+    for (r0, r1, c0, c1), b in zip(layout, blocks):
+        G = from_device(X[r0:r1, c0:c1])
+        e = O.rel_frobenius(G, O.orthogonalize(b, 4, None, "aol"))
+        worst = max(worst, e)
+        assert e <= BF16_TOL, (r0, c0, e)
+        X[r0:r1, c0:c1] = 0
+    log(f"{m} x {n}: worst block relF={worst:.3e}")
+    assert not bool((X != 0).any())
+    del X
+    torch.cuda.empty_cache()
+    tm.release_workspaces()
+
+
+def test_max_size_square_65536_block_diagonal():
+    """The largest matrix the library accepts: the update's Y operand spans
+    8 GiB, so row offsets past 4 GiB must not wrap."""
+    log("case: 65536 x 65536 bf16 block-diagonal, 256 blocks 256 x 256, AOL t=4")
+    _block_diagonal_case(65536, 65536, 256, 100)
+
+
+@pytest.mark.parametrize("m,n", [(65536, 40003), (40003, 65536)])
+def test_max_size_ragged_block_diagonal(m, n):
+    """One side at the maximum and a ragged other side (padded to a tile),
+    tall (transposed in and out) and wide."""
+    log(f"case: {m} x {n} bf16 block-diagonal, 128 blocks, AOL t=4")
+    _block_diagonal_case(m, n, 128, 300)
 
 
 def test_square_4096_batch_of_4_matches_single_calls():

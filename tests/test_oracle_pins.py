@@ -245,6 +245,46 @@ def test_p6_invariances(m, n):
 
 
 # --------------------------------------------------------------------------
+# Block-diagonal inputs: every product of the iteration (eq. ns_quintic) keeps
+# the block structure of X X^T, and the AOL scale of a row (Section 2.3)
+# only sums that row of the Gram, so the output is the block-diagonal of the
+# blocks' own outputs.  A global normalisation (Frobenius) couples the blocks.
+# --------------------------------------------------------------------------
+@pytest.mark.parametrize("m,n,count", [(40, 40, 4), (30, 52, 5), (61, 23, 3), (7, 9, 7)])
+def test_block_diagonal_input_gives_block_diagonal_output(m, n, count):
+    layout, blocks = synth.block_diagonal_blocks(m, n, count, 0.7, seed=11)
+    X = np.zeros((m, n))
+    for (r0, r1, c0, c1), B in zip(layout, blocks):
+        X[r0:r1, c0:c1] = B
+    for precond in ("aol", "none"):
+        Z = O.orthogonalize(X, 4, None, precond)
+        E = Z.copy()
+        for (r0, r1, c0, c1), B in zip(layout, blocks):
+            Zb = O.orthogonalize(B, 4, None, precond)
+            assert relF(Z[r0:r1, c0:c1], Zb) <= 1e-12, precond
+            E[r0:r1, c0:c1] = 0
+        assert np.max(np.abs(E)) <= 1e-14 * np.max(np.abs(Z)), precond
+    Zf = O.orthogonalize(X, 4, None, "frobenius")
+    r0, r1, c0, c1 = layout[0]
+    assert relF(Zf[r0:r1, c0:c1], O.orthogonalize(blocks[0], 4, None, "frobenius")) > 1e-3
+
+
+def test_block_diagonal_layout_partitions_and_orients():
+    for m, n, count in [(65536, 65536, 256), (65536, 40000, 128), (40000, 65536, 128), (5, 5, 5)]:
+        lay = synth.block_diagonal_layout(m, n, count)
+        assert len(lay) == count
+        assert lay[0][0] == 0 and lay[0][2] == 0 and lay[-1][1] == m and lay[-1][3] == n
+        for a, b in zip(lay, lay[1:]):
+            assert a[1] == b[0] and a[3] == b[2]
+        for r0, r1, c0, c1 in lay:
+            assert (m <= n) == (r1 - r0 <= c1 - c0)
+    with pytest.raises(ValueError):
+        synth.block_diagonal_layout(5, 4, 4)          # a square 1 x 1 block in a tall matrix
+    with pytest.raises(ValueError):
+        synth.block_diagonal_layout(4, 4, 5)
+
+
+# --------------------------------------------------------------------------
 # P7: Lemma 1, <G, PolarFactor(G S)> > 0, and the same for the t = 4 output
 # --------------------------------------------------------------------------
 @pytest.mark.parametrize("seed", range(4))
