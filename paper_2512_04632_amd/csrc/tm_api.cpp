@@ -365,8 +365,9 @@ tm_status plan_bf16(const Plan& pl, int iters, const float* coeffs, int precond,
     if (s == TM_OK && first && from_gram) s = gram_scale(pl, precond, part);
     if (s == TM_OK && scale)         // A1 = diag(s) A0 diag(s), one rounding
       s = launch(pl, tmk::kKindScaleA, 0, 0, 0, 0.f, 0.f, 0.f, 0u, 0);
+    // with `scale` the polynomial stores B~ diag(s) and the update reads X0
     if (s == TM_OK) s = launch(pl, tmk::kKindPoly, pcfg, 0, 0, a, b, c, scale, 0);
-    if (s == TM_OK) s = launch(pl, tmk::kKindUpdate, tcfg, src, dst, a, b, c, scale, 0);
+    if (s == TM_OK) s = launch(pl, tmk::kKindUpdate, tcfg, src, dst, a, b, c, 0u, 0);
     src = dst;
   }
   return s;

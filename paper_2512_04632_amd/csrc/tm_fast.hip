@@ -11,12 +11,13 @@
 //                 the fp32 accumulators are stored instead (A0 is rescaled
 //                 before rounding) and the epilogue emits the AOL row sums
 //                 sum_j |A0_ij| (eq. (aol))
-//   k_apply_s     A1 = diag(s) A0 diag(s) and X1 = diag(s) X0, each rounded
-//                 once to bf16
-//   k_poly_fast   B~ = b A + c A A + a I, upper tiles, mirrored store
+//   k_apply_s     A1 = diag(s) A0 diag(s), rounded once to bf16
+//   k_poly_fast   B~ = b A + c A A + a I, upper tiles, mirrored store; at
+//                 iteration 1 it stores C = B~ diag(s) instead, so that X1 =
+//                 diag(s) X0 is never formed: B~ X1 = C X0
 //   k_update_fast Y' = B~ Y = a Y + B Y: the axpy of the update rides on B~'s
 //                 diagonal, so the update is a single product with no second
-//                 read of Y
+//                 read of Y (iteration 1: Y' = C X0)
 //
 // Main loop: the 256 x 256 tile runs 8 wave64s (two per SIMD, so one wave's
 // barrier or DMA issue can hide behind the other's MFMAs) in a 2 x 4 grid of
@@ -34,6 +35,10 @@
 #include <stdint.h>
 
 #include "tm_internal.h"
+
+#ifndef TM_PP_BK
+#define TM_PP_BK 64
+#endif
 
 namespace tmk {
 namespace fast {
@@ -59,7 +64,7 @@ struct Tile {
 // of a ds_read_b128 pass (16 rows, one chunk) hit every bank once.
 template <int T, int BK>
 struct Ring {
-  static constexpr int NSTAGE = BK == 32 ? 4 : 3;
+  static constexpr int NSTAGE = BK == 32 ? 4 : (T == 256 ? 2 : 3);
   static constexpr int RB = 2 * BK;
   static constexpr int CPR = RB / 16;
   static constexpr int RPB = 256 / RB;
@@ -140,6 +145,8 @@ __device__ inline void dma_wait() {
   else if constexpr (PENDING == 4) asm volatile("s_waitcnt vmcnt(4)" ::: "memory");
   else if constexpr (PENDING == 8) asm volatile("s_waitcnt vmcnt(8)" ::: "memory");
   else if constexpr (PENDING == 12) asm volatile("s_waitcnt vmcnt(12)" ::: "memory");
+  else if constexpr (PENDING == 16) asm volatile("s_waitcnt vmcnt(16)" ::: "memory");
+  else if constexpr (PENDING == 24) asm volatile("s_waitcnt vmcnt(24)" ::: "memory");
   else static_assert(PENDING == 0, "unsupported in-flight count");
 }
 
@@ -345,26 +352,29 @@ __device__ inline void mainloop(f32x16_t (&acc)[Tile<T>::FM][Tile<T>::FN], char*
 
 // Ping-pong schedule for the 8-wave tile.  Waves 0-3 (group 0) and 4-7
 // (group 1) occupy one slot per SIMD each; group 1 runs one phase behind, so
-// that while one wave of a SIMD issues the 16 MFMAs of a K step from
+// that while one wave of a SIMD issues the 16 MFMAs of a 32-wide K step from
 // registers, the other issues its DMA and reads its operands of the next
 // step from LDS.  Every phase ends with a workgroup barrier:
-//   group 0: [MEM(j) | COMP(j)] for j = 0..nk-1, then one idle phase;
-//   group 1: one idle phase, then [MEM(j) | COMP(j)].
-// MEM(j) issues the DMA of stage j+S-1 (its buffer held stage j-1, whose
-// last reader, group 1's MEM(j-1), ended one barrier earlier) and reads
-// stage j.  Stage j+1 must be in LDS before group 0's MEM(j+1): group 0 waits
-// for its own DMA of that stage at the end of COMP(j), group 1 at the end of
-// MEM(j) (together with its LDS reads, so that stage j's buffer is free when
-// the next DMA into it is issued), both before the same barrier.
-template <int T, bool RM, bool SWAP>
+//   group 0: [MEM(h) | COMP(h)] for each 32-wide step h, then one idle phase;
+//   group 1: one idle phase, then [MEM(h) | COMP(h)].
+// The ring holds S stages of BK = 32 HPS elements of K, consumed in HPS
+// steps.  With BK = 64 a K-contiguous operand row of a stage is one full
+// 128-byte line, which the global -> LDS path moves at twice the rate of
+// the 64-byte half lines of BK = 32 (only two such stages fit in LDS).
+// The first step of stage j issues the DMA of stage j + S - 1 into the
+// buffer of stage j - 1, whose last reader (group 1's MEM of stage j - 1's
+// last step) ended one barrier earlier.  Stage j + 1 must be in LDS before
+// group 0's first MEM of it: in the last step of stage j, group 0 waits for
+// its own DMA of that stage at the end of its COMP, group 1 at the end of
+// its MEM (together with its LDS reads), both before the same barrier.
+template <int T, bool RM, bool SWAP, int BK>
 __device__ inline void mainloop_pp(f32x16_t (&acc)[Tile<T>::FM][Tile<T>::FN], char* smem,
                                    const uint16_t* a, int64_t lda, const uint16_t* b,
                                    int64_t ldb, int K) {
   static_assert(Tile<T>::NW == 8, "ping-pong needs two waves per SIMD");
-  constexpr int BK = 32, STAGES = 4;
   using R = Ring<T, BK>;
-  static_assert(R::NSTAGE == STAGES, "ring depth");
-  constexpr int PS = R::PER_STAGE;
+  constexpr int S = R::NSTAGE, PS = R::PER_STAGE, HPS = BK / 32;
+  static_assert(HPS * 32 == BK && S >= 2, "ring of 32-wide steps");
   const int wave = threadIdx.x >> 6;
   const int wm = wave / 4, wn = wave % 4;
   const bool g1 = __builtin_amdgcn_readfirstlane(wave) >= 4;
@@ -378,36 +388,39 @@ __device__ inline void mainloop_pp(f32x16_t (&acc)[Tile<T>::FM][Tile<T>::FN], ch
   const uint32_t lds0 = lds_addr(smem);
   const int nk = K / BK;
   auto issue = [&](int kt) {
-    const uint32_t st = lds0 + uint32_t((kt % STAGES) * R::STAGE);
+    const uint32_t st = lds0 + uint32_t((kt % S) * R::STAGE);
     issue_kc<T, BK>(a, lda, kt * BK, st);
     if constexpr (RM) issue_rm<T, BK>(b, ldb, kt * BK, st + R::A_BYTES);
     else issue_kc<T, BK>(b, ldb, kt * BK, st + R::A_BYTES);
   };
-  auto stage_ptr = [&](int kt) { return smem + (kt % STAGES) * R::STAGE; };
+  auto stage_ptr = [&](int kt) { return smem + (kt % S) * R::STAGE; };
 #pragma unroll
-  for (int s = 0; s + 1 < STAGES; ++s)
+  for (int s = 0; s + 1 < S; ++s)
     if (s < nk) issue(s);
-  ring_wait<PS>(min(nk - 1, STAGES - 2));
+  ring_wait<PS>(min(nk - 1, S - 2));
   if (g1) barrier_pinned();
 
   Frags<T> f0, f1;
   for (int j = 0; j < nk; ++j) {
-    // MEM(j)
-    if (j + STAGES - 1 < nk) issue(j + STAGES - 1);
     const char* st = stage_ptr(j);
-    load_frags<T, RM, BK>(f0, st, st + R::A_BYTES, 0, wm, wn);
-    load_frags<T, RM, BK>(f1, st, st + R::A_BYTES, 1, wm, wn);
-    const int pend = min(nk - 1, j + STAGES - 1) - (j + 1);
-    if (g1) {
-      __builtin_amdgcn_s_waitcnt(0xC07F);   // lgkmcnt(0)
-      dma_wait_stages<PS>(pend);
+    const int pend = min(nk - 1, j + S - 1) - (j + 1);
+#pragma unroll
+    for (int hs = 0; hs < HPS; ++hs) {
+      // MEM
+      if (hs == 0 && j + S - 1 < nk) issue(j + S - 1);
+      load_frags<T, RM, BK>(f0, st, st + R::A_BYTES, 2 * hs, wm, wn);
+      load_frags<T, RM, BK>(f1, st, st + R::A_BYTES, 2 * hs + 1, wm, wn);
+      if (g1) {
+        __builtin_amdgcn_s_waitcnt(0xC07F);   // lgkmcnt(0)
+        if (hs == HPS - 1) dma_wait_stages<PS>(pend);
+      }
+      barrier_pinned();
+      // COMP
+      mma<T, SWAP>(acc, f0);
+      mma<T, SWAP>(acc, f1);
+      if (!g1 && hs == HPS - 1) dma_wait_stages<PS>(pend);
+      barrier_pinned();
     }
-    barrier_pinned();
-    // COMP(j)
-    mma<T, SWAP>(acc, f0);
-    mma<T, SWAP>(acc, f1);
-    if (!g1) dma_wait_stages<PS>(pend);
-    barrier_pinned();
   }
   if (!g1) barrier_pinned();
   __builtin_amdgcn_s_waitcnt(0xC07F);
@@ -419,8 +432,7 @@ __device__ inline void run_mainloop(f32x16_t (&acc)[Tile<T>::FM][Tile<T>::FN], c
                                     const uint16_t* a, int64_t lda, const uint16_t* b,
                                     int64_t ldb, int K) {
   if constexpr (Tile<T>::NW == 8) {
-    static_assert(BK == 32, "the 8-wave tile runs 32-wide K steps");
-    mainloop_pp<T, RM, SWAP>(acc, smem, a, lda, b, ldb, K);
+    mainloop_pp<T, RM, SWAP, BK>(acc, smem, a, lda, b, ldb, K);
   } else {
     mainloop<T, RM, SWAP, BK>(acc, smem, a, lda, b, ldb, K);
   }
@@ -674,6 +686,68 @@ __device__ inline void epilogue_sym(const f32x16_t (&acc)[Tile<T>::FM][Tile<T>::
   if (I != J) store_cols<T>(st, D, ld, int64_t(I) * T, int64_t(J) * T);
 }
 
+// First polynomial after a scaling pre-conditioner: C = B~ diag(s), so that
+// the first update reads X0 itself (B~ X1 = B~ diag(s) X0).  C is not
+// symmetric: the mirror C[j][i] = B~_ij s_i and the tile C[i][j] = B~_ij s_j
+// of the upper tile (I, J) differ.  Both are rounded once from the fp32 B~_ij;
+// the first goes through the stage while the second waits in registers as
+// packed bf16, then takes the stage in a second pass.
+template <int T, class Fv>
+__device__ inline void epilogue_sym_scaled(const f32x16_t (&acc)[Tile<T>::FM][Tile<T>::FN],
+                                           char* st, uint16_t* D, int64_t ld, int I, int J, Fv f,
+                                           const float* __restrict__ s) {
+  constexpr int FM = Tile<T>::FM, FN = Tile<T>::FN;
+  const int wm = wave_m(Tile<T>::NW), wn = wave_n(Tile<T>::NW);
+  uint2 keep[FM][FN][4];
+#pragma unroll
+  for (int fm = 0; fm < FM; ++fm) {
+    // s of this lane's 16 rows of the 32-row block fm (4 runs of 4 rows)
+    float4 si[4];
+#pragma unroll
+    for (int v4 = 0; v4 < 4; ++v4)
+      si[v4] = *reinterpret_cast<const float4*>(s + I * T + acc_row<T>(wm, fm, 4 * v4));
+#pragma unroll
+    for (int fn = 0; fn < FN; ++fn) {
+      const int c = acc_col<T>(wn, fn);
+      const float sj = s[J * T + c];
+#pragma unroll
+      for (int v4 = 0; v4 < 4; ++v4) {
+        const int r0 = acc_row<T>(wm, fm, 4 * v4);
+        char* p = st + c * Stage<T>::RS + r0 * 2;
+        const uint2 old = *reinterpret_cast<const uint2*>(p);
+        const uint16_t* o = reinterpret_cast<const uint16_t*>(&old);
+        const float sv[4] = {si[v4].x, si[v4].y, si[v4].z, si[v4].w};
+        uint16_t out[4], out2[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          const float x = f(r0 + u, c, acc[fm][fn][4 * v4 + u], o[u]);
+          out[u] = f2bf(x * sv[u]);
+          out2[u] = f2bf(x * sj);
+        }
+        *reinterpret_cast<uint2*>(p) = *reinterpret_cast<const uint2*>(out);
+        keep[fm][fn][v4] = *reinterpret_cast<const uint2*>(out2);
+      }
+    }
+    __builtin_amdgcn_sched_barrier(0);   // keeps the loads of the next block here
+  }
+  __syncthreads();
+  store_rows<T>(st, D, ld, int64_t(J) * T, int64_t(I) * T);   // C[j][i], j in J, i in I
+  if (I == J) return;
+  __syncthreads();
+#pragma unroll
+  for (int fm = 0; fm < FM; ++fm)
+#pragma unroll
+    for (int fn = 0; fn < FN; ++fn) {
+      const int c = acc_col<T>(wn, fn);
+#pragma unroll
+      for (int v4 = 0; v4 < 4; ++v4)
+        *reinterpret_cast<uint2*>(st + c * Stage<T>::RS + acc_row<T>(wm, fm, 4 * v4) * 2) =
+            keep[fm][fn][v4];
+    }
+  __syncthreads();
+  store_cols<T>(st, D, ld, int64_t(I) * T, int64_t(J) * T);   // C[i][j]
+}
+
 // fp32 store of a symmetric tile and its mirror straight from the registers
 // (first Gram only).
 template <int T>
@@ -780,7 +854,7 @@ __global__ __launch_bounds__(Tile<T>::NT) void k_gram_fast(const Phase P) {
 
 // B~ = b A + c A A + a I (upper tiles, mirrored).  The stage is preloaded with
 // A's tile (J, I), whose element (j, i) equals A_ij.
-template <int T, int BK>
+template <int T, int BK, bool SCALED>
 __global__ __launch_bounds__(Tile<T>::NT) void k_poly_fast(const Phase P) {
   __shared__ __attribute__((aligned(1024))) char smem[smem_bytes<T, BK>()];
   constexpr int FM = Tile<T>::FM, FN = Tile<T>::FN;
@@ -803,7 +877,10 @@ __global__ __launch_bounds__(Tile<T>::NT) void k_poly_fast(const Phase P) {
   auto f = [=](int i, int j, float x, uint16_t aij) {
     return b * bf2f(aij) + c * x + ((diag && i == j) ? a : 0.f);
   };
-  epilogue_sym<T>(acc, smem, B, ldg, I, J, f);
+  if constexpr (SCALED)   // kScale: a separate kernel, so that neither epilogue spills
+    epilogue_sym_scaled<T>(acc, smem, B, ldg, I, J, f, reinterpret_cast<const float*>(w + WL.s));
+  else
+    epilogue_sym<T>(acc, smem, B, ldg, I, J, f);
 }
 
 // Y' = B~ Y.  The operands are fed transposed so that each lane holds 4
@@ -920,34 +997,20 @@ __global__ __launch_bounds__(256) void k_load_in(const Phase P) {
 __global__ __launch_bounds__(256) void k_apply_s(const Phase P) {
   const Loc L = locate(P, blockIdx.x);
   const Entry& E = P.e[L.ent];
-  const int64_t kp = E.kp, Np = E.Np;
+  const int64_t kp = E.kp;
   char* w = ws_of(P, E, L.mat);
   const WsLayout WL = ws_layout(E.kp, E.Np, 2);
   const float* s = reinterpret_cast<const float*>(w + WL.s);
-  const int nA = int((kp * kp + kElemBlock - 1) / kElemBlock);
-  if (L.tile < nA) {
-    const int64_t idx = int64_t(L.tile) * kElemBlock + int64_t(threadIdx.x) * 8;
-    if (idx >= kp * kp) return;
-    const float* A0 = reinterpret_cast<const float*>(w + WL.a32);
-    uint16_t* A = reinterpret_cast<uint16_t*>(w + WL.a);
-    const int64_t i = idx / kp, j = idx - i * kp;   // kp % 8 == 0: the 8 stay in row i
-    const float si = s[i];
-    uint16_t o[8];
-#pragma unroll
-    for (int e = 0; e < 8; ++e) o[e] = f2bf(A0[idx + e] * (si * s[j + e]));
-    *reinterpret_cast<uint4*>(A + i * WL.ldg + j) = *reinterpret_cast<const uint4*>(o);
-    return;
-  }
-  const int64_t idx = int64_t(L.tile - nA) * kElemBlock + int64_t(threadIdx.x) * 8;
-  if (idx >= kp * Np) return;
-  const int64_t i = idx / Np, l = idx - i * Np;   // Np % 8 == 0: the 8 stay in row i
-  uint16_t* Y = wbuf(P, E, L.mat, kSlotFirst) + i * WL.ldy + l;
+  const int64_t idx = int64_t(L.tile) * kElemBlock + int64_t(threadIdx.x) * 8;
+  if (idx >= kp * kp) return;
+  const float* A0 = reinterpret_cast<const float*>(w + WL.a32);
+  uint16_t* A = reinterpret_cast<uint16_t*>(w + WL.a);
+  const int64_t i = idx / kp, j = idx - i * kp;   // kp % 8 == 0: the 8 stay in row i
   const float si = s[i];
-  uint4 v = *reinterpret_cast<const uint4*>(Y);
-  uint16_t* e = reinterpret_cast<uint16_t*>(&v);
+  uint16_t o[8];
 #pragma unroll
-  for (int u = 0; u < 8; ++u) e[u] = f2bf(bf2f(e[u]) * si);
-  *reinterpret_cast<uint4*>(Y) = v;
+  for (int e = 0; e < 8; ++e) o[e] = f2bf(A0[idx + e] * (si * s[j + e]));
+  *reinterpret_cast<uint4*>(A + i * WL.ldg + j) = *reinterpret_cast<const uint4*>(o);
 }
 
 #define TM_LAUNCH(kern) \
@@ -957,7 +1020,9 @@ template <int T, int BK>
 static hipError_t launch_t(int kind, const Phase& P, hipStream_t st) {
   switch (kind) {
     case kKindGram: TM_LAUNCH((k_gram_fast<T, BK>));
-    case kKindPoly: TM_LAUNCH((k_poly_fast<T, BK>));
+    case kKindPoly:
+      if (P.flags & kScale) TM_LAUNCH((k_poly_fast<T, BK, true>));
+      TM_LAUNCH((k_poly_fast<T, BK, false>));
     case kKindUpdate: TM_LAUNCH((k_update_fast<T, BK>));
   }
   return hipErrorInvalidValue;
@@ -976,7 +1041,7 @@ hipError_t launch_fast_bf16(int kind, int cfg, bool wide, const Phase& P, hipStr
     return hipGetLastError();
   }
   switch (cfg_tile(cfg)) {
-    case 256: return fast::launch_t<256, 32>(kind, P, st);
+    case 256: return fast::launch_t<256, TM_PP_BK>(kind, P, st);
     case 128:
       return wide ? fast::launch_t<128, wide_k_step(128)>(kind, P, st)
                   : fast::launch_t<128, 32>(kind, P, st);

@@ -39,7 +39,8 @@ constexpr int kSlotAlt2 = 2;
 constexpr int kSlotFinal = 3;
 
 // Phase flags.
-constexpr uint32_t kScale = 1u;   // first iteration after AOL / Frobenius: apply s
+constexpr uint32_t kScale = 1u;   // first iteration after AOL / Frobenius: apply s (bf16
+                                  // polynomial: store B~ diag(s))
 constexpr uint32_t kRowSum = 2u;  // Gram epilogue emits AOL row-sum partials
 constexpr uint32_t kFrob = 4u;    // AOL-vector kernel: uniform s from the Frobenius partials
 constexpr uint32_t kA32 = 8u;     // Gram stores A0 in fp32 (first iteration, before scaling)
@@ -140,9 +141,7 @@ TM_HD uint32_t blocks_per_matrix(int kind, int cfg, uint32_t k, uint32_t N, uint
     case kKindUpdate: return cdiv(kp, T) * cdiv(Np, T);
     case kKindApplyScale:
     case kKindCopyOut: return uint32_t((uint64_t(k) * N + kElemBlock - 1) / kElemBlock);
-    case kKindScaleA:
-      return uint32_t((uint64_t(kp) * kp + kElemBlock - 1) / kElemBlock +
-                      (uint64_t(kp) * Np + kElemBlock - 1) / kElemBlock);
+    case kKindScaleA: return uint32_t((uint64_t(kp) * kp + kElemBlock - 1) / kElemBlock);
   }
   return 0;
 }
