@@ -158,15 +158,20 @@ def main(argv=None) -> int:
 
     ms_per_step = elapsed_ms / args.steps
     step_flops = 0
-    upd_flops_per_launch = 0
+    upd_flops_per_iter = 0
     for count, m, n, _ in entries:
         fl = alg_flops(min(m, n), max(m, n), args.iters)
         step_flops += fl["total"] * count
-        upd_flops_per_launch += fl["update_per_iter"] * count
+        upd_flops_per_iter += fl["update_per_iter"] * count
     tflops = step_flops / (ms_per_step * 1e-3) / 1e12
     upd_ms, upd_n = phases["update"]
     upd_avg_ms = upd_ms / upd_n if upd_n else None
-    upd_tflops = upd_flops_per_launch / (upd_avg_ms * 1e-3) / 1e12 if upd_n else None
+    # a call with more than 64 matrices (or a split last wave) runs an
+    # iteration's update as several launches: average over all of them
+    upd_flops_total = upd_flops_per_iter * args.iters * args.steps
+    upd_flops_per_launch = (upd_flops_total // upd_n if upd_n and upd_flops_total % upd_n == 0
+                            else (upd_flops_total / upd_n if upd_n else 0))
+    upd_tflops = upd_flops_total / (upd_ms * 1e-3) / 1e12 if upd_n else None
     peak = PEAK_BF16_TFLOPS if dtype == "bf16" else PEAK_F32_TFLOPS
 
     config = {"workload": args.workload, "matrices": n_mat,
