@@ -22,10 +22,10 @@
 // Main loop: the 256 x 256 tile runs 8 wave64s (two per SIMD, so one wave's
 // barrier or DMA issue can hide behind the other's MFMAs) in a 2 x 4 grid of
 // 128 x 64 blocks; smaller tiles run 4 waves in a 2 x 2 grid.  Each wave
-// accumulates 32 x 32 v_mfma_f32_32x32x16_bf16 blocks.  K
-// advances 32 elements per stage through a 4-stage LDS ring filled by
-// global_load_lds_dwordx4 (direct to LDS, no VGPR staging), three stages in
-// flight.  K-contiguous operands are stored as 64-byte rows with the 16-byte
+// accumulates 32 x 32 v_mfma_f32_32x32x16_bf16 blocks.  Operands reach LDS
+// through global_load_lds_dwordx4 (direct to LDS, no VGPR staging) into a
+// ring of stages: two of 64 K elements for the 256 tile, four of 32 (or three
+// of 64 / 128 in single-wave launches) for the smaller ones.  K-contiguous operands are stored as 64-byte rows with the 16-byte
 // chunk index XOR ((row / 4) % 4); the update's Y operand is staged in its
 // row-major layout (32 rows of T bf16) with 32-byte chunks XOR-swizzled per
 // row and read with ds_read_b64_tr_b16, which hands each lane 4 consecutive
@@ -173,18 +173,21 @@ __device__ inline void barrier_pinned() {
 // One instruction fills 1 KB = 64 / CPR rows; lane i writes chunk i % CPR of
 // its row, i.e. it loads logical chunk (i % CPR) ^ swizzle.
 template <int T, int BK>
-__device__ inline void issue_kc(const uint16_t* src, int64_t ld, int k0, uint32_t lds) {
+__device__ inline void dma_kc(const uint16_t* src, int64_t ld, int k0, uint32_t lds, int q) {
   using R = Ring<T, BK>;
   constexpr int RPI = 64 / R::CPR;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int j = wave + Tile<T>::NW * q;
+  const int r = j * RPI + lane / R::CPR;
+  const int c = (lane % R::CPR) ^ ((r / R::RPB) % R::CPR);
+  const uint32_t voff = uint32_t((int64_t(r) * ld + k0 + c * 8) * 2);
+  dma16(src, voff, __builtin_amdgcn_readfirstlane(lds + uint32_t(j) * 1024u));
+}
+
+template <int T, int BK>
+__device__ inline void issue_kc(const uint16_t* src, int64_t ld, int k0, uint32_t lds) {
 #pragma unroll
-  for (int q = 0; q < R::DMA_OP; ++q) {
-    const int j = wave + Tile<T>::NW * q;
-    const int r = j * RPI + lane / R::CPR;
-    const int c = (lane % R::CPR) ^ ((r / R::RPB) % R::CPR);
-    const uint32_t voff = uint32_t((int64_t(r) * ld + k0 + c * 8) * 2);
-    dma16(src, voff, __builtin_amdgcn_readfirstlane(lds + uint32_t(j) * 1024u));
-  }
+  for (int q = 0; q < Ring<T, BK>::DMA_OP; ++q) dma_kc<T, BK>(src, ld, k0, lds, q);
 }
 
 // 32-byte chunk swizzle of the row-major Y stage (row = 2T bytes).
@@ -197,21 +200,24 @@ __device__ inline int swz_y(int r) {
 // The stage's first row goes into the 64-bit base address, so the 32-bit
 // per-lane offset spans BK rows only, whatever the matrix size.
 template <int T, int BK>
-__device__ inline void issue_rm(const uint16_t* src, int64_t ld, int k0, uint32_t lds) {
+__device__ inline void dma_rm(const uint16_t* src, int64_t ld, int k0, uint32_t lds, int q) {
   constexpr int ROWB = 2 * T;
   constexpr int LPR = ROWB / 16;          // lanes per row
   constexpr int RPI = 1024 / ROWB;        // rows per instruction
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const uint16_t* base = src + int64_t(k0) * ld;
+  const int j = wave + Tile<T>::NW * q;
+  const int r = j * RPI + lane / LPR;
+  const int p16 = lane % LPR;
+  const int c = (p16 >> 1) ^ swz_y<T>(r);
+  const uint32_t voff = uint32_t((int64_t(r) * ld + c * 16 + (p16 & 1) * 8) * 2);
+  dma16(base, voff, __builtin_amdgcn_readfirstlane(lds + uint32_t(j) * 1024u));
+}
+
+template <int T, int BK>
+__device__ inline void issue_rm(const uint16_t* src, int64_t ld, int k0, uint32_t lds) {
 #pragma unroll
-  for (int q = 0; q < Ring<T, BK>::DMA_OP; ++q) {
-    const int j = wave + Tile<T>::NW * q;
-    const int r = j * RPI + lane / LPR;
-    const int p16 = lane % LPR;
-    const int c = (p16 >> 1) ^ swz_y<T>(r);
-    const uint32_t voff = uint32_t((int64_t(r) * ld + c * 16 + (p16 & 1) * 8) * 2);
-    dma16(base, voff, __builtin_amdgcn_readfirstlane(lds + uint32_t(j) * 1024u));
-  }
+  for (int q = 0; q < Ring<T, BK>::DMA_OP; ++q) dma_rm<T, BK>(src, ld, k0, lds, q);
 }
 
 // ---------------------------------------------------------------- compute
@@ -282,24 +288,26 @@ __device__ inline void mma(f32x16_t (&acc)[Tile<T>::FM][Tile<T>::FN], const Frag
     }
 }
 
-// acc = A (T x K, K-contiguous rows of a) * B^T where B's rows are the
-// K-contiguous rows of b (RM = false) or B = the K x T row-major block of b
-// (RM = true).  K is a multiple of BK; every tile is full.
-//
-// Schedule per stage kt (BK / 16 K slices of 16): the operands of slice 0
-// were read before the stage began; every slice's operands are read while
-// the previous slice's MFMAs run; before the last slice's MFMAs the ring is
-// synchronised for stage kt+1 (its DMA done in every wave, and every wave
-// done reading stage kt), the DMA of stage kt + NSTAGE reuses stage kt's
-// buffer, and slice 0 of stage kt+1 is read while the last slice's MFMAs run.
-// The K slices are consumed in increasing order whatever BK is, so every
-// output element accumulates the same products in the same order.
+// 4-wave main loop.  acc = A (T x K, K-contiguous rows of a) * B^T where B's
+// rows are the K-contiguous rows of b (RM = false) or B = the K x T row-major
+// block of b (RM = true); K is a multiple of BK and every tile is full.  The
+// operands of each 16-wide K slice are read from LDS while the previous
+// slice's MFMAs run.  The DMA is spread over the K slices: while stage kt is
+// read and multiplied, each wave issues its share of stage kt + NSTAGE - 1,
+// PS / NS instructions per slice, into the buffer of stage kt - 1 (every wave
+// finished reading it before the barrier that opened stage kt).  The
+// global -> LDS path (about 64 bytes per clock and compute unit) is then fed
+// evenly instead of in one burst per stage that stalls every wave.  Slices
+// are consumed in increasing order whatever BK is, so every output element
+// accumulates the same products in the same order.
 template <int T, bool RM, bool SWAP, int BK>
 __device__ inline void mainloop(f32x16_t (&acc)[Tile<T>::FM][Tile<T>::FN], char* smem,
-                                const uint16_t* a, int64_t lda, const uint16_t* b, int64_t ldb,
-                                int K) {
+                                const uint16_t* a, int64_t lda, const uint16_t* b,
+                                int64_t ldb, int K) {
   using R = Ring<T, BK>;
-  constexpr int PS = R::PER_STAGE, NS = BK / 16, NST = R::NSTAGE;
+  constexpr int PS = R::PER_STAGE, NS = BK / 16, NST = R::NSTAGE, DO = R::DMA_OP;
+  constexpr int PPS = PS / NS;
+  static_assert(PPS * NS == PS && PPS >= 1, "whole DMA instructions per slice");
   const int wave = threadIdx.x >> 6;
   const int wm = wave / (Tile<T>::NW / 2), wn = wave % (Tile<T>::NW / 2);
 #pragma unroll
@@ -311,36 +319,51 @@ __device__ inline void mainloop(f32x16_t (&acc)[Tile<T>::FM][Tile<T>::FN], char*
 
   const uint32_t lds0 = lds_addr(smem);
   const int nk = K / BK;
-  auto issue = [&](int kt) {
-    const uint32_t st = lds0 + uint32_t((kt % NST) * R::STAGE);
-    issue_kc<T, BK>(a, lda, kt * BK, st);
-    if constexpr (RM) issue_rm<T, BK>(b, ldb, kt * BK, st + R::A_BYTES);
-    else issue_kc<T, BK>(b, ldb, kt * BK, st + R::A_BYTES);
+  auto stage_lds = [&](int kt) { return lds0 + uint32_t((kt % NST) * R::STAGE); };
+  // DMA instruction i (0 .. PS - 1) of stage kt: operand a first, then b
+  auto dma_one = [&](int kt, int i) {
+    if (i < DO) {
+      dma_kc<T, BK>(a, lda, kt * BK, stage_lds(kt), i);
+    } else {
+      if constexpr (RM) dma_rm<T, BK>(b, ldb, kt * BK, stage_lds(kt) + R::A_BYTES, i - DO);
+      else dma_kc<T, BK>(b, ldb, kt * BK, stage_lds(kt) + R::A_BYTES, i - DO);
+    }
   };
   auto stage_ptr = [&](int kt) { return smem + (kt % NST) * R::STAGE; };
 #pragma unroll
-  for (int s = 0; s < NST; ++s)
-    if (s < nk) issue(s);
-  ring_wait<PS>(min(nk - 1, NST - 1));
+  for (int s = 0; s + 1 < NST; ++s)
+    if (s < nk)
+      for (int i = 0; i < PS; ++i) dma_one(s, i);
+  ring_wait<PS>(min(nk - 1, NST - 2));
 
   Frags<T> f0, f1;
   load_frags<T, RM, BK>(f0, stage_ptr(0), stage_ptr(0) + R::A_BYTES, 0, wm, wn);
   for (int kt = 0; kt < nk; ++kt) {
     const char* st = stage_ptr(kt);
+    const int nx = kt + NST - 1;   // stage refilled during this one
+    const bool fill = nx < nk;
 #pragma unroll
     for (int s = 0; s < NS; s += 2) {
       load_frags<T, RM, BK>(f1, st, st + R::A_BYTES, s + 1, wm, wn);
+      if (fill)
+#pragma unroll
+        for (int i = 0; i < PPS; ++i) dma_one(nx, s * PPS + i);
       mma<T, SWAP>(acc, f0);
       if (s + 2 < NS) {
         load_frags<T, RM, BK>(f0, st, st + R::A_BYTES, s + 2, wm, wn);
+        if (fill)
+#pragma unroll
+          for (int i = 0; i < PPS; ++i) dma_one(nx, (s + 1) * PPS + i);
         mma<T, SWAP>(acc, f1);
       } else {
+        if (fill)
+#pragma unroll
+          for (int i = 0; i < PPS; ++i) dma_one(nx, (s + 1) * PPS + i);
         __builtin_amdgcn_sched_barrier(0);
         if (kt + 1 < nk) {
           ring_wait<PS>(min(nk - 1, kt + NST - 1) - (kt + 1));
-          if (kt + NST < nk) issue(kt + NST);
-          const char* nx = stage_ptr(kt + 1);
-          load_frags<T, RM, BK>(f0, nx, nx + R::A_BYTES, 0, wm, wn);
+          const char* nxp = stage_ptr(kt + 1);
+          load_frags<T, RM, BK>(f0, nxp, nxp + R::A_BYTES, 0, wm, wn);
         }
         __builtin_amdgcn_sched_barrier(0);
         mma<T, SWAP>(acc, f1);
