@@ -62,6 +62,10 @@ def main(argv=None) -> int:
                     help="leave the library's per-launch event hooks off in the timed region "
                          "(no phase split and no roofline figure; the step time then carries no "
                          "event-recording overhead, which matters for small workloads)")
+    ap.add_argument("--graph", action="store_true",
+                    help="capture one step into a HIP graph (torch.cuda.graph, on a side "
+                         "stream warmed up first) and time its replays; implies "
+                         "--no-phase-timing")
     ap.add_argument("--optimizer", action="store_true",
                     help="time the optimizer step (tm_muon_step_grouped: momentum, bf16 "
                          "orthogonalization, fp32 parameter update) over the workload's matrices "
@@ -141,13 +145,33 @@ def main(argv=None) -> int:
         run(batches)
     torch.cuda.synchronize()
 
+    step = lambda: run(batches)  # noqa: E731
+    if args.graph:
+        # The library keeps its workspace per (device, stream): one call on the
+        # capture stream sizes it, so the captured call allocates nothing.
+        args.no_phase_timing = True
+        side = torch.cuda.Stream(dev)
+        side.wait_stream(stream)
+        with torch.cuda.stream(side):
+            run(batches)
+        side.synchronize()
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph, stream=side):
+            run(batches)
+        torch.cuda.synchronize()
+        for _ in range(max(1, args.warmup)):
+            graph.replay()
+        torch.cuda.synchronize()
+        step = graph.replay
+        progress("captured one step into a graph")
+
     tm.timing_reset()
     tm.timing_enable(not args.no_phase_timing)
     start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     start.record(stream)
     for _ in range(args.steps):
-        run(batches)
+        step()
     stop.record(stream)
     torch.cuda.synchronize()
     tm.timing_enable(False)
@@ -178,6 +202,8 @@ def main(argv=None) -> int:
               "shapes": [[c, m, n] for c, m, n, _ in entries],
               "alpha": [a for _, _, _, a in entries], "iters": args.iters,
               "precond": args.precond, "call": "grouped" if grouped else "batched"}
+    if args.graph:
+        config["launch"] = "hip graph replay"
     result = {
         "metric": f"orthogonalized matrices/s ({PRECOND_NAME[args.precond]} + {args.iters} NS iterations)",
         "value": round(n_mat * args.steps / (elapsed_ms * 1e-3), 3),

@@ -33,6 +33,13 @@
  * Calls on different streams may run concurrently; calls that overlap on the
  * same stream are ordered by the stream.
  *
+ * Graph capture.  A call on a stream whose workspace is already large enough
+ * (an earlier call of the same or larger shapes on that stream) allocates
+ * nothing and synchronises nothing, so it can be captured into a HIP graph;
+ * the captured kernels keep that workspace's address.  While such a graph is
+ * in use, make no larger call on the capturing stream (growing the workspace
+ * frees the old one) and do not call tm_release_workspaces().
+ *
  * Errors.  Arguments are validated before anything is enqueued; an invalid
  * call returns a negative status and leaves memory untouched.  Failures of the
  * HIP runtime return TM_ERR_HIP.  tm_last_error() gives a thread-local message
