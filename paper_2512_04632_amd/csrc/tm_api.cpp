@@ -207,9 +207,6 @@ constexpr int kWave = 256;
 // K of the launch is a multiple of the step: the Gram contracts over Np, the
 // polynomial and the update over kp.
 bool wide_step_ok(int kind, int cfg, const Phase& P) {
-#ifdef TM_NO_WIDE_K_STEP
-  return false;
-#endif
   const uint32_t step = uint32_t(tmk::wide_k_step(tmk::cfg_tile(cfg)));
   if (step == 32u || P.total > kWave) return false;
   for (int e = 0; e < P.nent; ++e) {

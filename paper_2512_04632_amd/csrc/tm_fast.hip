@@ -25,9 +25,10 @@
 // accumulates 32 x 32 v_mfma_f32_32x32x16_bf16 blocks.  Operands reach LDS
 // through global_load_lds_dwordx4 (direct to LDS, no VGPR staging) into a
 // ring of stages: two of 64 K elements for the 256 tile, four of 32 (or three
-// of 64 / 128 in single-wave launches) for the smaller ones.  K-contiguous operands are stored as 64-byte rows with the 16-byte
-// chunk index XOR ((row / 4) % 4); the update's Y operand is staged in its
-// row-major layout (32 rows of T bf16) with 32-byte chunks XOR-swizzled per
+// of 64 / 128 in single-wave launches) for the smaller ones.  K-contiguous
+// operands are stored as rows of 2 BK bytes whose 16-byte chunks are
+// XOR-swizzled by row group; the update's Y operand is staged in its
+// row-major layout (BK rows of T bf16) with 32-byte chunks XOR-swizzled per
 // row and read with ds_read_b64_tr_b16, which hands each lane 4 consecutive
 // K values of one column.  Both layouts are free of LDS bank conflicts for
 // the reads.
@@ -36,12 +37,11 @@
 
 #include "tm_internal.h"
 
-#ifndef TM_PP_BK
-#define TM_PP_BK 64
-#endif
-
 namespace tmk {
 namespace fast {
+
+// K elements per ring stage of the 8-wave (256) tile: rows of 128 bytes.
+constexpr int kPingPongBK = 64;
 
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x16_t __attribute__((ext_vector_type(16)));
@@ -1064,7 +1064,7 @@ hipError_t launch_fast_bf16(int kind, int cfg, bool wide, const Phase& P, hipStr
     return hipGetLastError();
   }
   switch (cfg_tile(cfg)) {
-    case 256: return fast::launch_t<256, TM_PP_BK>(kind, P, st);
+    case 256: return fast::launch_t<256, fast::kPingPongBK>(kind, P, st);
     case 128:
       return wide ? fast::launch_t<128, wide_k_step(128)>(kind, P, st)
                   : fast::launch_t<128, 32>(kind, P, st);
