@@ -54,10 +54,6 @@ def main(argv=None) -> int:
     ap.add_argument("--copy-calibration-mb", type=int, default=0,
                     help="after the timed region, run one plain device copy of this many MiB "
                          "(reference kernel for scaling the FETCH_SIZE / WRITE_SIZE counters)")
-    ap.add_argument("--accuracy", type=int, default=0, metavar="N",
-                    help="instead of timing: polar error of the GPU result and of the fp64 oracle "
-                         "for t = 1..6 iterations and the Frobenius / Schatten-4 / AOL "
-                         "pre-conditionings on an N x N N(0,1) matrix (bf16)")
     ap.add_argument("--no-phase-timing", action="store_true",
                     help="leave the library's per-launch event hooks off in the timed region "
                          "(no phase split and no roofline figure; the step time then carries no "
@@ -86,9 +82,6 @@ def main(argv=None) -> int:
 
     from paper_2512_04632_amd import _lib as tm
     from paper_2512_04632_amd import synth
-
-    if args.accuracy:
-        return _accuracy_sweep(args.accuracy)
 
     if args.workload not in synth.WORKLOADS:
         print(f"bench.py: unknown workload {args.workload!r}; choose from "
@@ -331,32 +324,6 @@ def _bench_optimizer(args, batches, entries, dev, stream, progress):
         if phases["opt_momentum"] + phases["opt_apply"] > 0 else None,
     }
     print(json.dumps(result), flush=True)
-    return 0
-
-
-def _accuracy_sweep(n):
-    """Polar error against the number of iterations, GPU (bf16) and oracle (fp64)."""
-    import numpy as np
-    import torch
-
-    from oracle import turbomuon as O
-    from paper_2512_04632_amd import _lib as tm
-    from paper_2512_04632_amd import synth
-    X = synth.cast(synth.gaussian_matrix(n, n, seed=0), "bf16")
-    Q = O.polar_factor(X)
-    rows = []
-    for pre in ("frobenius", "schatten4", "aol"):
-        for t in range(1, 7):
-            g = torch.from_numpy(X.astype(np.float32)).to(torch.bfloat16).cuda()
-            tm.orthogonalize(g, t, None, pre)
-            torch.cuda.synchronize()
-            G = g.float().cpu().numpy().astype(np.float64)
-            R = O.orthogonalize(X, t, None, pre)
-            rows.append({"precond": pre, "iters": t, "eps_polar_gpu": round(O.eps_polar(G, X, Q), 4),
-                         "eps_polar_oracle": round(O.eps_polar(R, X, Q), 4),
-                         "rel_frobenius": round(O.rel_frobenius(G, R), 5)})
-    print(json.dumps({"metric": "polar error vs iterations", "matrix": f"{n}x{n} N(0,1) bf16, seed 0",
-                      "coefficients": "constant (3.4445, -4.7750, 2.0315)", "rows": rows}), flush=True)
     return 0
 
 
