@@ -175,12 +175,14 @@ int choose_tile_cfg(const std::vector<Item>& items) {
 }
 
 // bf16 Gram and polynomial phases: the layout tile T (kp, Np multiples of
-// it) is halved, down to 64, while the phase has fewer than two waves of
-// tiles for the 256 compute units; these phases have about k^2 / T^2 / 2
-// tiles per matrix against k N / T^2 for the update.
-int choose_sym_cfg(int kind, int tcfg, const std::vector<Item>& items) {
+// it) is halved, down to 64 (or 32 with `small`: one-wave tiles, not for the
+// first Gram, whose row partials cover 64 columns), while the phase has fewer
+// than two waves of tiles for the 256 compute units; these phases have about
+// k^2 / T^2 / 2 tiles per matrix against k N / T^2 for the update.
+int choose_sym_cfg(int kind, int tcfg, const std::vector<Item>& items, bool small = false) {
   int cfg = tcfg;
-  while (cfg < tmk::kNumCfg - 1) {
+  const int last = small ? tmk::kCfgSym32 : tmk::kNumCfg - 1;
+  while (cfg < last) {
     uint64_t tiles = 0;
     for (const Item& it : items)
       tiles += uint64_t(it.count) * tmk::blocks_per_matrix(kind, cfg, it.k, it.N, it.kp, it.Np);
@@ -208,7 +210,9 @@ constexpr int kWave = 256;
 // polynomial and the update over kp.
 bool wide_step_ok(int kind, int cfg, const Phase& P) {
   const uint32_t step = uint32_t(tmk::wide_k_step(tmk::cfg_tile(cfg)));
-  if (step == 32u || P.total > kWave) return false;
+  // the 32 tile's ring (48 KB) leaves room for three blocks per compute unit
+  const int limit = tmk::cfg_tile(cfg) == 32 ? 3 * kWave : kWave;
+  if (step == 32u || P.total > limit) return false;
   for (int e = 0; e < P.nent; ++e) {
     const uint32_t K = kind == tmk::kKindGram ? P.e[e].Np : P.e[e].kp;
     if (P.e[e].tiles_per != 0u && K % step != 0u) return false;
@@ -329,8 +333,9 @@ tm_status plan_bf16(const Plan& pl, int iters, const float* coeffs, int precond,
   const bool from_gram = precond == TM_PRECOND_AOL || precond == TM_PRECOND_SCHATTEN4;
   const bool scaled = from_gram || frob;
   const uint32_t rflags = first_gram_flags(precond);
-  const int gcfg = choose_sym_cfg(tmk::kKindGram, tcfg, *pl.items);
-  const int pcfg = choose_sym_cfg(tmk::kKindPoly, tcfg, *pl.items);
+  const int gcfg1 = choose_sym_cfg(tmk::kKindGram, tcfg, *pl.items);   // with row partials
+  const int gcfg = choose_sym_cfg(tmk::kKindGram, tcfg, *pl.items, true);
+  const int pcfg = choose_sym_cfg(tmk::kKindPoly, tcfg, *pl.items, true);
   const int part = tmk::kMinTile;   // the matrix-core Gram emits row partials per 64 columns
   tm_status s = TM_OK;
   if (iters > 0 || from_gram)
@@ -342,7 +347,7 @@ tm_status plan_bf16(const Plan& pl, int iters, const float* coeffs, int precond,
   if (s != TM_OK) return s;
   if (iters == 0) {
     if (from_gram) {
-      s = launch(pl, tmk::kKindGram, gcfg, tmk::kSlotFirst, 0, 0.f, 0.f, 0.f, rflags | tmk::kA32, 0);
+      s = launch(pl, tmk::kKindGram, gcfg1, tmk::kSlotFirst, 0, 0.f, 0.f, 0.f, rflags | tmk::kA32, 0);
       if (s == TM_OK) s = gram_scale(pl, precond, part);
       if (s != TM_OK) return s;
     }
@@ -358,7 +363,7 @@ tm_status plan_bf16(const Plan& pl, int iters, const float* coeffs, int precond,
     const bool first = it == 1;
     const uint32_t scale = (first && scaled) ? tmk::kScale : 0u;
     const uint32_t gflags = (first ? rflags : 0u) | (scale ? tmk::kA32 : 0u);
-    s = launch(pl, tmk::kKindGram, gcfg, src, 0, 0.f, 0.f, 0.f, gflags, 0);
+    s = launch(pl, tmk::kKindGram, gflags != 0u ? gcfg1 : gcfg, src, 0, 0.f, 0.f, 0.f, gflags, 0);
     if (s == TM_OK && first && from_gram) s = gram_scale(pl, precond, part);
     if (s == TM_OK && scale)         // A1 = diag(s) A0 diag(s), one rounding
       s = launch(pl, tmk::kKindScaleA, 0, 0, 0, 0.f, 0.f, 0.f, 0u, 0);

@@ -47,13 +47,15 @@ typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x16_t __attribute__((ext_vector_type(16)));
 typedef short s16x4_t __attribute__((ext_vector_type(4)));
 
-// Tile T x T computed by NW wave64s in a 2 x (NW/2) grid; each wave owns
-// (T/2) x (2T/NW) of the output as 32 x 32 MFMA blocks.
+// Tile T x T computed by NW wave64s in a WGM x WGN grid (2 x 4, 2 x 2, or a
+// single wave for the 32 tile); each wave owns TWM x TWN of the output as
+// 32 x 32 MFMA blocks.
 template <int T>
 struct Tile {
-  static constexpr int NW = T == 256 ? 8 : 4;   // 2 waves per SIMD for the large tile
+  static constexpr int NW = T == 256 ? 8 : (T == 32 ? 1 : 4);   // 2 waves per SIMD for 256
+  static constexpr int WGM = NW == 1 ? 1 : 2, WGN = NW / WGM;
   static constexpr int NT = 64 * NW;            // threads per workgroup
-  static constexpr int TWM = T / 2, TWN = 2 * T / NW;
+  static constexpr int TWM = T / WGM, TWN = T / WGN;
   static constexpr int FM = TWM / 32, FN = TWN / 32;
 };
 
@@ -127,14 +129,22 @@ __device__ inline void ring_sync() {
 }
 
 // Wait for all but `stages` of this wave's stages in flight, then barrier.
-template <int PS>
+// (MAXS: the most stages a caller can leave in flight; larger counts are not
+// instantiated, since vmcnt holds at most 63.)
+template <int PS, int MAXS>
 __device__ inline void ring_wait(int stages) {
+  static_assert(MAXS * PS <= 63, "in-flight count beyond vmcnt");
   __builtin_amdgcn_s_waitcnt(0xC07F);   // lgkmcnt(0), vmcnt/expcnt untouched
-  if (stages >= 4) ring_sync_dma<4 * PS>();
-  else if (stages == 3) ring_sync_dma<3 * PS>();
-  else if (stages == 2) ring_sync_dma<2 * PS>();
-  else if (stages == 1) ring_sync_dma<PS>();
-  else ring_sync_dma<0>();
+  if constexpr (MAXS >= 3) {
+    if (stages >= 3) { ring_sync_dma<3 * PS>(); return; }
+  }
+  if constexpr (MAXS >= 2) {
+    if (stages == 2) { ring_sync_dma<2 * PS>(); return; }
+  }
+  if constexpr (MAXS >= 1) {
+    if (stages == 1) { ring_sync_dma<PS>(); return; }
+  }
+  ring_sync_dma<0>();
 }
 
 // DMA-only wait (no barrier): at most PENDING DMA instructions of this wave
@@ -309,7 +319,7 @@ __device__ inline void mainloop(f32x16_t (&acc)[Tile<T>::FM][Tile<T>::FN], char*
   constexpr int PPS = PS / NS;
   static_assert(PPS * NS == PS && PPS >= 1, "whole DMA instructions per slice");
   const int wave = threadIdx.x >> 6;
-  const int wm = wave / (Tile<T>::NW / 2), wn = wave % (Tile<T>::NW / 2);
+  const int wm = wave / Tile<T>::WGN, wn = wave % Tile<T>::WGN;
 #pragma unroll
   for (int fm = 0; fm < Tile<T>::FM; ++fm)
 #pragma unroll
@@ -334,7 +344,7 @@ __device__ inline void mainloop(f32x16_t (&acc)[Tile<T>::FM][Tile<T>::FN], char*
   for (int s = 0; s + 1 < NST; ++s)
     if (s < nk)
       for (int i = 0; i < PS; ++i) dma_one(s, i);
-  ring_wait<PS>(min(nk - 1, NST - 2));
+  ring_wait<PS, NST - 2>(min(nk - 1, NST - 2));
 
   Frags<T> f0, f1;
   load_frags<T, RM, BK>(f0, stage_ptr(0), stage_ptr(0) + R::A_BYTES, 0, wm, wn);
@@ -361,7 +371,7 @@ __device__ inline void mainloop(f32x16_t (&acc)[Tile<T>::FM][Tile<T>::FN], char*
           for (int i = 0; i < PPS; ++i) dma_one(nx, (s + 1) * PPS + i);
         __builtin_amdgcn_sched_barrier(0);
         if (kt + 1 < nk) {
-          ring_wait<PS>(min(nk - 1, kt + NST - 1) - (kt + 1));
+          ring_wait<PS, NST - 2>(min(nk - 1, kt + NST - 1) - (kt + 1));
           const char* nxp = stage_ptr(kt + 1);
           load_frags<T, RM, BK>(f0, nxp, nxp + R::A_BYTES, 0, wm, wn);
         }
@@ -420,7 +430,7 @@ __device__ inline void mainloop_pp(f32x16_t (&acc)[Tile<T>::FM][Tile<T>::FN], ch
 #pragma unroll
   for (int s = 0; s + 1 < S; ++s)
     if (s < nk) issue(s);
-  ring_wait<PS>(min(nk - 1, S - 2));
+  ring_wait<PS, S - 2>(min(nk - 1, S - 2));
   if (g1) barrier_pinned();
 
   Frags<T> f0, f1;
@@ -557,8 +567,8 @@ template <int T>
 __device__ inline int acc_col(int wn, int fn) {
   return wn * Tile<T>::TWN + fn * 32 + (threadIdx.x & 31);
 }
-__device__ inline int wave_m(int nw) { return int(threadIdx.x >> 6) / (nw / 2); }
-__device__ inline int wave_n(int nw) { return int(threadIdx.x >> 6) % (nw / 2); }
+__device__ inline int wave_m(int wgn) { return int(threadIdx.x >> 6) / wgn; }
+__device__ inline int wave_n(int wgn) { return int(threadIdx.x >> 6) % wgn; }
 
 // ---------------------------------------------------------------- epilogues
 // Output tiles are staged through LDS (the ring is free after the main loop)
@@ -686,7 +696,7 @@ __device__ inline void load_rows(char* st, const uint16_t* src, int64_t ld, int6
 template <int T, class Fv>
 __device__ inline void epilogue_sym(const f32x16_t (&acc)[Tile<T>::FM][Tile<T>::FN], char* st,
                                     uint16_t* D, int64_t ld, int I, int J, Fv f) {
-  const int wm = wave_m(Tile<T>::NW), wn = wave_n(Tile<T>::NW);
+  const int wm = wave_m(Tile<T>::WGN), wn = wave_n(Tile<T>::WGN);
 #pragma unroll
   for (int fm = 0; fm < Tile<T>::FM; ++fm)
 #pragma unroll
@@ -720,7 +730,7 @@ __device__ inline void epilogue_sym_scaled(const f32x16_t (&acc)[Tile<T>::FM][Ti
                                            char* st, uint16_t* D, int64_t ld, int I, int J, Fv f,
                                            const float* __restrict__ s) {
   constexpr int FM = Tile<T>::FM, FN = Tile<T>::FN;
-  const int wm = wave_m(Tile<T>::NW), wn = wave_n(Tile<T>::NW);
+  const int wm = wave_m(Tile<T>::WGN), wn = wave_n(Tile<T>::WGN);
   uint2 keep[FM][FN][4];
 #pragma unroll
   for (int fm = 0; fm < FM; ++fm) {
@@ -776,7 +786,7 @@ __device__ inline void epilogue_sym_scaled(const f32x16_t (&acc)[Tile<T>::FM][Ti
 template <int T>
 __device__ inline void store_sym_f32(const f32x16_t (&acc)[Tile<T>::FM][Tile<T>::FN], float* D,
                                      int64_t ld, int I, int J) {
-  const int wm = wave_m(Tile<T>::NW), wn = wave_n(Tile<T>::NW);
+  const int wm = wave_m(Tile<T>::WGN), wn = wave_n(Tile<T>::WGN);
 #pragma unroll
   for (int fm = 0; fm < Tile<T>::FM; ++fm)
 #pragma unroll
@@ -820,7 +830,8 @@ __global__ __launch_bounds__(Tile<T>::NT) void k_gram_fast(const Phase P) {
     epilogue_sym<T>(acc, smem, reinterpret_cast<uint16_t*>(w + WL.a), WL.ldg, I, J, f);
   }
 
-  if (P.flags & kRowSum) {
+  // The host never asks a 32 tile for row sums (their partials cover 64 columns).
+  if (T >= kMinTile && (P.flags & kRowSum)) {
     // part[b][i] = sum over the 64 columns of block b of |A0_ij| (with kRowSq:
     // A0_ij^2, whose total is ||A0||_F^2 for the Schatten-4 scale), from the fp32
     // accumulators.  The reduction tree is fixed for every tile size: each
@@ -837,7 +848,7 @@ __global__ __launch_bounds__(Tile<T>::NT) void k_gram_fast(const Phase P) {
     float* rs = reinterpret_cast<float*>(smem);       // [NB][T] row sums over 32-column blocks
     float* cs = rs + NB * T;                          // [NB][T] column sums over 32-row blocks
     const int lane = threadIdx.x & 63;
-    const int wm = wave_m(Tile<T>::NW), wn = wave_n(Tile<T>::NW);
+    const int wm = wave_m(Tile<T>::WGN), wn = wave_n(Tile<T>::WGN);
 #pragma unroll
     for (int fm = 0; fm < FM; ++fm)
 #pragma unroll
@@ -945,7 +956,7 @@ __global__ __launch_bounds__(Tile<T>::NT) void k_update_fast(const Phase P) {
   // acc[fm][fn] element v: output row i = wm*TWM + fm*32 + lane%32, columns
   // l0..l0+3 with l0 = wn*TWN + fn*32 + 8(v/4) + 4(lane/32)
   const int lane = threadIdx.x & 63;
-  const int wm = wave_m(Tile<T>::NW), wn = wave_n(Tile<T>::NW);
+  const int wm = wave_m(Tile<T>::WGN), wn = wave_n(Tile<T>::WGN);
 #pragma unroll
   for (int fm = 0; fm < FM; ++fm)
 #pragma unroll
@@ -1046,7 +1057,9 @@ static hipError_t launch_t(int kind, const Phase& P, hipStream_t st) {
     case kKindPoly:
       if (P.flags & kScale) TM_LAUNCH((k_poly_fast<T, BK, true>));
       TM_LAUNCH((k_poly_fast<T, BK, false>));
-    case kKindUpdate: TM_LAUNCH((k_update_fast<T, BK>));
+    case kKindUpdate:
+      if constexpr (T >= 64) TM_LAUNCH((k_update_fast<T, BK>));   // layout tiles only
+      break;
   }
   return hipErrorInvalidValue;
 }
@@ -1071,6 +1084,10 @@ hipError_t launch_fast_bf16(int kind, int cfg, bool wide, const Phase& P, hipStr
     case 64:
       return wide ? fast::launch_t<64, wide_k_step(64)>(kind, P, st)
                   : fast::launch_t<64, 32>(kind, P, st);
+    case 32:
+      if (kind == kKindUpdate || (kind == kKindGram && (P.flags & kRowSum))) break;
+      return wide ? fast::launch_t<32, wide_k_step(32)>(kind, P, st)
+                  : fast::launch_t<32, 32>(kind, P, st);
   }
   return hipErrorInvalidValue;
 }
