@@ -20,7 +20,7 @@
 
 namespace tmk {
 hipError_t launch_elementwise_bf16(int kind, const Phase& P, hipStream_t st);
-hipError_t launch_fast_bf16(int kind, int cfg, bool wide, const Phase& P, hipStream_t st);
+hipError_t launch_fast_bf16(int kind, int cfg, int step, const Phase& P, hipStream_t st);
 hipError_t launch_phase_f32(int kind, int cfg, const Phase& P, hipStream_t st);
 hipError_t launch_opt(int apply, const OptPhase& P, hipStream_t st);
 }  // namespace tmk
@@ -203,21 +203,25 @@ struct Plan {
 // Compute units of the MI355X: the blocks of one full wave of the large tiles.
 constexpr int kWave = 256;
 
-// The wide K step of a bf16 matrix-core launch: only for launches of at most
-// one wave of blocks (its larger ring holds one workgroup per compute unit,
-// which a launch with more blocks than units would feel), and only when every
-// K of the launch is a multiple of the step: the Gram contracts over Np, the
-// polynomial and the update over kp.
-bool wide_step_ok(int kind, int cfg, const Phase& P) {
-  const uint32_t step = uint32_t(tmk::wide_k_step(tmk::cfg_tile(cfg)));
-  // the 32 tile's ring (48 KB) leaves room for three blocks per compute unit
-  const int limit = tmk::cfg_tile(cfg) == 32 ? 3 * kWave : kWave;
-  if (step == 32u || P.total > limit) return false;
-  for (int e = 0; e < P.nent; ++e) {
+// K step (elements per ring stage) of a 4-wave or one-wave bf16 launch: the
+// widest whose ring still lets the launch's blocks be resident together —
+// 96 KB rings (128 for the 64 tile, 64 for the 128 tile) hold one block per
+// compute unit, so only for launches of at most one wave of blocks; 48 KB
+// rings (64 for the 64 tile, 128 for the 32 tile) hold three, so for up to
+// three waves; else 32.  Every K of the launch must be a multiple of the
+// step: the Gram contracts over Np, the polynomial and the update over kp.
+// (The 256 tile's ping-pong ring is fixed.)
+int k_step(int kind, int cfg, const Phase& P) {
+  const int T = tmk::cfg_tile(cfg);
+  int step = 32;
+  if (T == 128 && P.total <= kWave) step = 64;
+  if (T == 64) step = P.total <= kWave ? 128 : (P.total <= 3 * kWave ? 64 : 32);
+  if (T == 32 && P.total <= 3 * kWave) step = 128;
+  for (int e = 0; e < P.nent && step > 32; ++e) {
     const uint32_t K = kind == tmk::kKindGram ? P.e[e].Np : P.e[e].kp;
-    if (P.e[e].tiles_per != 0u && K % step != 0u) return false;
+    if (P.e[e].tiles_per != 0u && K % uint32_t(step) != 0u) step = 32;
   }
-  return true;
+  return step;
 }
 
 // Enqueue one kernel launch of a prepared phase descriptor (timed when the
@@ -235,7 +239,7 @@ tm_status fire(const Plan& pl, int kind, int cfg, const Phase& P) {
   else if (kind == tmk::kKindFrob || kind == tmk::kKindAolVector || kind == tmk::kKindApplyScale)
     e = tmk::launch_elementwise_bf16(kind, P, pl.st);
   else
-    e = tmk::launch_fast_bf16(kind, cfg, wide_step_ok(kind, cfg, P), P, pl.st);
+    e = tmk::launch_fast_bf16(kind, cfg, k_step(kind, cfg, P), P, pl.st);
   if (tl.start) {
     (void)hipEventRecord(tl.stop, pl.st);
     g_timed.push_back(tl);

@@ -1066,7 +1066,7 @@ static hipError_t launch_t(int kind, const Phase& P, hipStream_t st) {
 
 }  // namespace fast
 
-hipError_t launch_fast_bf16(int kind, int cfg, bool wide, const Phase& P, hipStream_t st) {
+hipError_t launch_fast_bf16(int kind, int cfg, int step, const Phase& P, hipStream_t st) {
   if (P.total <= 0) return hipSuccess;
   if (kind == kKindLoadIn) {
     hipLaunchKernelGGL(fast::k_load_in, dim3(P.total), dim3(256), 0, st, P);
@@ -1079,15 +1079,14 @@ hipError_t launch_fast_bf16(int kind, int cfg, bool wide, const Phase& P, hipStr
   switch (cfg_tile(cfg)) {
     case 256: return fast::launch_t<256, fast::kPingPongBK>(kind, P, st);
     case 128:
-      return wide ? fast::launch_t<128, wide_k_step(128)>(kind, P, st)
-                  : fast::launch_t<128, 32>(kind, P, st);
+      return step == 64 ? fast::launch_t<128, 64>(kind, P, st) : fast::launch_t<128, 32>(kind, P, st);
     case 64:
-      return wide ? fast::launch_t<64, wide_k_step(64)>(kind, P, st)
-                  : fast::launch_t<64, 32>(kind, P, st);
+      return step == 128 ? fast::launch_t<64, 128>(kind, P, st)
+             : step == 64 ? fast::launch_t<64, 64>(kind, P, st)
+                          : fast::launch_t<64, 32>(kind, P, st);
     case 32:
       if (kind == kKindUpdate || (kind == kKindGram && (P.flags & kRowSum))) break;
-      return wide ? fast::launch_t<32, wide_k_step(32)>(kind, P, st)
-                  : fast::launch_t<32, 32>(kind, P, st);
+      return step == 128 ? fast::launch_t<32, 128>(kind, P, st) : fast::launch_t<32, 32>(kind, P, st);
   }
   return hipErrorInvalidValue;
 }

@@ -114,11 +114,6 @@ constexpr int kNumCfg = 3;
 constexpr int kCfgSym32 = 3;
 TM_HD int cfg_tile(int cfg) { return cfg == 0 ? 256 : (cfg == 1 ? 128 : (cfg == 2 ? 64 : 32)); }
 
-// K step of the wide-step variant of the bf16 matrix-core kernels of a tile
-// size (the 256 tile always steps 32): small tiles do few MFMAs per K slice,
-// so stages of 64 or 128 K elements cut the barriers and waits per MFMA.  A
-// launch takes it when every matrix's K is a multiple of it.
-TM_HD constexpr int wide_k_step(int T) { return T <= 64 ? 128 : (T == 128 ? 64 : 32); }
 
 // Logical blocks per matrix of each kernel.
 // The numbering matches the TM_PHASE_* timing phases of turbomuon.h.
