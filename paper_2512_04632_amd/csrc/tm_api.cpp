@@ -203,20 +203,19 @@ struct Plan {
 // Compute units of the MI355X: the blocks of one full wave of the large tiles.
 constexpr int kWave = 256;
 
-// K step (elements per ring stage) of a 4-wave or one-wave bf16 launch: the
-// widest whose ring still lets the launch's blocks be resident together —
-// 96 KB rings (128 for the 64 tile, 64 for the 128 tile) hold one block per
-// compute unit, so only for launches of at most one wave of blocks; 48 KB
-// rings (64 for the 64 tile, 128 for the 32 tile) hold three, so for up to
-// three waves; else 32.  Every K of the launch must be a multiple of the
-// step: the Gram contracts over Np, the polynomial and the update over kp.
-// (The 256 tile's ping-pong ring is fixed.)
+// K step (elements per ring stage) of a 4-wave or one-wave bf16 launch.  A
+// 96 KB ring (128 for the 64 tile, 64 for the 128 tile) holds one block per
+// compute unit, so it serves launches of at most one wave of blocks; a 48 KB
+// ring (64 for the 64 tile, 128 for the 32 tile) holds three, which suits a
+// launch of any size; else 32 (the 128 tile's many-block launches).  Every K
+// of the launch must be a multiple of the step: the Gram contracts over Np,
+// the polynomial and the update over kp.  (The 256 tile's ring is fixed.)
 int k_step(int kind, int cfg, const Phase& P) {
   const int T = tmk::cfg_tile(cfg);
   int step = 32;
   if (T == 128 && P.total <= kWave) step = 64;
-  if (T == 64) step = P.total <= kWave ? 128 : (P.total <= 3 * kWave ? 64 : 32);
-  if (T == 32 && P.total <= 3 * kWave) step = 128;
+  if (T == 64) step = P.total <= kWave ? 128 : 64;
+  if (T == 32) step = 128;
   for (int e = 0; e < P.nent && step > 32; ++e) {
     const uint32_t K = kind == tmk::kKindGram ? P.e[e].Np : P.e[e].kp;
     if (P.e[e].tiles_per != 0u && K % uint32_t(step) != 0u) step = 32;
