@@ -59,14 +59,16 @@ struct Tile {
   static constexpr int FM = TWM / 32, FN = TWN / 32;
 };
 
-// LDS ring of one main loop: NSTAGE stages of BK K-elements of both operands.
+// LDS ring of one main loop: NSTAGE stages of BK K-elements of both operands
+// (the 128 tile's 32-wide ring is 3 deep, 48 KB, so that three blocks share a
+// compute unit in many-block launches).
 // A K-contiguous operand row of a stage is RB = 2 BK bytes, stored as CPR
 // 16-byte chunks; logical chunk c of row r lives at chunk c ^ ((r / RPB) %
 // CPR), RPB being the rows that span the 64 banks once, so that the 16 lanes
 // of a ds_read_b128 pass (16 rows, one chunk) hit every bank once.
 template <int T, int BK>
 struct Ring {
-  static constexpr int NSTAGE = BK == 32 ? 4 : (T == 256 ? 2 : 3);
+  static constexpr int NSTAGE = BK == 32 ? (T == 128 ? 3 : 4) : (T == 256 ? 2 : 3);
   static constexpr int RB = 2 * BK;
   static constexpr int CPR = RB / 16;
   static constexpr int RPB = 256 / RB;
