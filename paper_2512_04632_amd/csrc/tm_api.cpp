@@ -444,9 +444,9 @@ tm_status run_locked(std::vector<Item>& items, int esz, int iters, const float* 
     tcfg = choose_tile_cfg(items);
     for (Item& it : items) {
       tmk::tiled_dims(it.k, it.N, uint32_t(tmk::cfg_tile(tcfg)), &it.kp, &it.Np);
-      // A wide matrix that needs no padding is read in place by iteration 1
-      // (and scaled there in place); a single iteration would read and write
-      // the caller's buffer in the same launch, so it keeps the copy.
+      // A wide matrix that needs no padding is read in place by iteration 1;
+      // a single iteration would read and write the caller's buffer in the
+      // same launch, so it keeps the copy.
       it.direct = !it.tall && it.kp == it.k && it.Np == it.N && iters != 1 &&
                   (reinterpret_cast<uintptr_t>(it.x) & 15u) == 0u;
     }
