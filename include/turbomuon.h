@@ -31,7 +31,9 @@
  * (device, stream), grown on first use with hipMalloc and kept until
  * tm_release_workspaces() or process exit; growing it synchronises `stream`.
  * Calls on different streams may run concurrently; calls that overlap on the
- * same stream are ordered by the stream.
+ * same stream are ordered by the stream.  The cache is keyed by the stream
+ * handle: synchronise a stream before destroying it, since a stream created
+ * later may receive the same handle and reuse that workspace.
  *
  * Graph capture.  A call on a stream whose workspace is already large enough
  * (an earlier call of the same or larger shapes on that stream) allocates
@@ -166,7 +168,8 @@ tm_status tm_release_workspaces(void);
 #define TM_PHASE_APPLY_SCALE   6  /* iters = 0: X1 = diag(s) X0 */
 #define TM_PHASE_COPY_OUT      7  /* iters = 1: result copied into the caller's buffer */
 #define TM_PHASE_LOAD_IN       8  /* bf16: X (or X^T) copied into the zero-padded workspace */
-#define TM_PHASE_SCALE_A       9  /* bf16: A1 = diag(s) A0 diag(s) and X1 = diag(s) X0 */
+#define TM_PHASE_SCALE_A       9  /* bf16: A1 = diag(s) A0 diag(s) (X1 is never stored: the first
+                                    polynomial keeps B~ diag(s) and the update reads X0) */
 #define TM_PHASE_OPT_MOMENTUM 10  /* optimizer step: momentum and the bf16 matrix to orthogonalize */
 #define TM_PHASE_OPT_APPLY    11  /* optimizer step: parameter update */
 #define TM_NUM_PHASES         12
