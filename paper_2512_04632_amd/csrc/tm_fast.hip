@@ -154,7 +154,9 @@ __device__ inline void ring_wait(int stages) {
 template <int PENDING>
 __device__ inline void dma_wait() {
   if constexpr (PENDING == 0) asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  else if constexpr (PENDING == 2) asm volatile("s_waitcnt vmcnt(2)" ::: "memory");
   else if constexpr (PENDING == 4) asm volatile("s_waitcnt vmcnt(4)" ::: "memory");
+  else if constexpr (PENDING == 6) asm volatile("s_waitcnt vmcnt(6)" ::: "memory");
   else if constexpr (PENDING == 8) asm volatile("s_waitcnt vmcnt(8)" ::: "memory");
   else if constexpr (PENDING == 12) asm volatile("s_waitcnt vmcnt(12)" ::: "memory");
   else if constexpr (PENDING == 16) asm volatile("s_waitcnt vmcnt(16)" ::: "memory");
@@ -462,11 +464,114 @@ __device__ inline void mainloop_pp(f32x16_t (&acc)[Tile<T>::FM][Tile<T>::FN], ch
   dma_wait<0>();   // nothing is in flight here; keeps the counter model exact
 }
 
+// Ping-pong schedule of the update (operand b = the K x T row-major block of
+// Y).  A stage of b splits into two halves of BK / 2 rows without shortening
+// its 2T-byte row pieces, so the DMA can be spread evenly over the two steps
+// of a stage instead of issued in the first: the first step of stage j
+// issues operand a of stage j + 1, the second issues the second half of b's
+// stage j + 1 and the first half of b's stage j + 2.  That last half goes
+// into the buffer of stage j, whose first half every wave finished reading
+// in the first step (the first step reads K rows 0 .. BK/2 - 1 of b, the
+// second the others; group 1's reads are complete at the barrier that ends
+// its memory phase, group 0's before its compute phase).  Every step ends
+// with the same wait protocol as mainloop_pp, for exactly the data the next
+// step reads; the DMAs issued after that data stay in flight:
+//   end of step 1 of stage j: b's second half of stage j is needed; b's
+//     first half of j + 1 and a of j + 1 (HB + DO instructions) may be pending;
+//   end of step 2: a of j + 1 and b's first half of j + 1 are needed; b's
+//     second half of j + 1 and first half of j + 2 (HB each) may be pending.
+template <int T, bool SWAP, int BK>
+__device__ inline void mainloop_pp_rm(f32x16_t (&acc)[Tile<T>::FM][Tile<T>::FN], char* smem,
+                                      const uint16_t* a, int64_t lda, const uint16_t* b,
+                                      int64_t ldb, int K) {
+  static_assert(Tile<T>::NW == 8, "ping-pong needs two waves per SIMD");
+  using R = Ring<T, BK>;
+  constexpr int S = R::NSTAGE, DO = R::DMA_OP, HB = DO / 2;
+  static_assert(S == 2 && BK == 64, "two stages of two 32-wide steps");
+  static_assert(HB == 2 && Tile<T>::NW * HB * (1024 / (2 * T)) == BK / 2,
+                "dma_rm instructions 0 .. HB-1 of every wave cover the first BK / 2 rows");
+  const int wave = threadIdx.x >> 6;
+  const int wm = wave / 4, wn = wave % 4;
+  const bool g1 = __builtin_amdgcn_readfirstlane(wave) >= 4;
+#pragma unroll
+  for (int fm = 0; fm < Tile<T>::FM; ++fm)
+#pragma unroll
+    for (int fn = 0; fn < Tile<T>::FN; ++fn)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) acc[fm][fn][v] = 0.f;
+
+  const uint32_t lds0 = lds_addr(smem);
+  const int nk = K / BK;
+  auto stage_lds = [&](int kt) { return lds0 + uint32_t((kt % S) * R::STAGE); };
+  auto issue_a = [&](int kt) { issue_kc<T, BK>(a, lda, kt * BK, stage_lds(kt)); };
+  auto issue_b = [&](int kt, int half) {
+#pragma unroll
+    for (int q = 0; q < HB; ++q) dma_rm<T, BK>(b, ldb, kt * BK, stage_lds(kt) + R::A_BYTES, half * HB + q);
+  };
+  auto stage_ptr = [&](int kt) { return smem + (kt % S) * R::STAGE; };
+  // wait at the end of step hs of stage j for what step hs + 1 (or stage j + 1) reads
+  auto wait_step = [&](int j, int hs) {
+    if (hs == 0) {
+      if (j + 1 < nk) dma_wait<HB + DO>();
+      else dma_wait<0>();
+    } else {
+      if (j + 2 < nk) dma_wait<2 * HB>();
+      else if (j + 1 < nk) dma_wait<HB>();
+      else dma_wait<0>();
+    }
+  };
+
+  issue_a(0);
+  issue_b(0, 0);
+  issue_b(0, 1);
+  if (nk > 1) {
+    issue_b(1, 0);
+    __builtin_amdgcn_s_waitcnt(0xC07F);
+    ring_sync_dma<HB>();
+  } else {
+    __builtin_amdgcn_s_waitcnt(0xC07F);
+    ring_sync_dma<0>();
+  }
+  if (g1) barrier_pinned();
+
+  Frags<T> f0, f1;
+  for (int j = 0; j < nk; ++j) {
+    const char* st = stage_ptr(j);
+#pragma unroll
+    for (int hs = 0; hs < 2; ++hs) {
+      // MEM
+      if (hs == 0) {
+        if (j + 1 < nk) issue_a(j + 1);
+      } else {
+        if (j + 1 < nk) issue_b(j + 1, 1);
+        if (j + 2 < nk) issue_b(j + 2, 0);
+      }
+      load_frags<T, true, BK>(f0, st, st + R::A_BYTES, 2 * hs, wm, wn);
+      load_frags<T, true, BK>(f1, st, st + R::A_BYTES, 2 * hs + 1, wm, wn);
+      if (g1) {
+        __builtin_amdgcn_s_waitcnt(0xC07F);   // lgkmcnt(0)
+        wait_step(j, hs);
+      }
+      barrier_pinned();
+      // COMP
+      mma<T, SWAP>(acc, f0);
+      mma<T, SWAP>(acc, f1);
+      if (!g1) wait_step(j, hs);
+      barrier_pinned();
+    }
+  }
+  if (!g1) barrier_pinned();
+  __builtin_amdgcn_s_waitcnt(0xC07F);
+  dma_wait<0>();
+}
+
 template <int T, bool RM, bool SWAP, int BK>
 __device__ inline void run_mainloop(f32x16_t (&acc)[Tile<T>::FM][Tile<T>::FN], char* smem,
                                     const uint16_t* a, int64_t lda, const uint16_t* b,
                                     int64_t ldb, int K) {
-  if constexpr (Tile<T>::NW == 8) {
+  if constexpr (Tile<T>::NW == 8 && RM) {
+    mainloop_pp_rm<T, SWAP, BK>(acc, smem, a, lda, b, ldb, K);
+  } else if constexpr (Tile<T>::NW == 8) {
     mainloop_pp<T, RM, SWAP, BK>(acc, smem, a, lda, b, ldb, K);
   } else {
     mainloop<T, RM, SWAP, BK>(acc, smem, a, lda, b, ldb, K);
@@ -905,7 +1010,14 @@ __global__ __launch_bounds__(Tile<T>::NT) void k_poly_fast(const Phase P) {
   uint16_t* B = reinterpret_cast<uint16_t*>(w + WL.b);
   const int64_t ldg = WL.ldg;
   f32x16_t acc[FM][FN];
-  run_mainloop<T, false, false, BK>(acc, smem, A + int64_t(I) * T * ldg, ldg, A + int64_t(J) * T * ldg, ldg, kp);
+  // A is stored exactly symmetric (mirrored stores of the same values), so
+  // the K x T row-major block of its columns J holds the rows J: the 8-wave
+  // tile reads that operand row-major, which lets its ping-pong spread the
+  // DMA over both steps of a stage.  The MFMA operands are the same values.
+  if constexpr (Tile<T>::NW == 8)
+    run_mainloop<T, true, false, BK>(acc, smem, A + int64_t(I) * T * ldg, ldg, A + int64_t(J) * T, ldg, kp);
+  else
+    run_mainloop<T, false, false, BK>(acc, smem, A + int64_t(I) * T * ldg, ldg, A + int64_t(J) * T * ldg, ldg, kp);
   load_rows<T>(smem, A, ldg, int64_t(J) * T, int64_t(I) * T);
   __syncthreads();
   const float a = P.a, b = P.b, c = P.c;
