@@ -24,13 +24,15 @@
 // 128 x 64 blocks; smaller tiles run 4 waves in a 2 x 2 grid.  Each wave
 // accumulates 32 x 32 v_mfma_f32_32x32x16_bf16 blocks.  Operands reach LDS
 // through global_load_lds_dwordx4 (direct to LDS, no VGPR staging) into a
-// ring of stages: two of 64 K elements for the 256 tile, four of 32 (or three
-// of 64 / 128 in single-wave launches) for the smaller ones.  K-contiguous
+// ring of stages: two of 64 K elements for the 256 tile (five operand slots
+// of 64 K elements for its Gram), three or four of 32, 64 or 128 for the
+// smaller ones.  K-contiguous
 // operands are stored as rows of 2 BK bytes whose 16-byte chunks are
-// XOR-swizzled by row group; the update's Y operand is staged in its
-// row-major layout (BK rows of T bf16) with 32-byte chunks XOR-swizzled per
-// row and read with ds_read_b64_tr_b16, which hands each lane 4 consecutive
-// K values of one column.  Both layouts are free of LDS bank conflicts for
+// XOR-swizzled by row group; the update's Y operand (and on the 256 tile the
+// polynomial's second A operand) is staged in its row-major layout (BK rows
+// of T bf16) with 32-byte chunks XOR-swizzled per row and read with
+// ds_read_b64_tr_b16, which hands each lane 4 consecutive K values of one
+// column.  Both layouts are free of LDS bank conflicts for
 // the reads.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
@@ -74,7 +76,8 @@ struct Ring {
   static constexpr int RPB = 256 / RB;
   static constexpr int A_BYTES = T * RB;         // one operand stage
   static constexpr int STAGE = 2 * A_BYTES;
-  static constexpr int LDS = NSTAGE * STAGE;
+  // the 256 tile's Gram keeps five operand slots of A_BYTES (mainloop_pp_kc5)
+  static constexpr int LDS = T == 256 ? 5 * A_BYTES : NSTAGE * STAGE;
   static constexpr int DMA_OP = T * BK / 512 / Tile<T>::NW;   // 1 KB DMAs per wave per operand
   static constexpr int PER_STAGE = 2 * DMA_OP;
   static_assert(T * BK % (512 * Tile<T>::NW) == 0, "whole DMA instructions per wave");
@@ -387,82 +390,24 @@ __device__ inline void mainloop(f32x16_t (&acc)[Tile<T>::FM][Tile<T>::FN], char*
   ring_sync<0>();   // the ring is free for the epilogue
 }
 
-// Ping-pong schedule for the 8-wave tile.  Waves 0-3 (group 0) and 4-7
-// (group 1) occupy one slot per SIMD each; group 1 runs one phase behind, so
-// that while one wave of a SIMD issues the 16 MFMAs of a 32-wide K step from
-// registers, the other issues its DMA and reads its operands of the next
-// step from LDS.  Every phase ends with a workgroup barrier:
+// Ping-pong schedule of the 8-wave tile (two loops below, one per layout of
+// operand b).  Waves 0-3 (group 0) and 4-7 (group 1) occupy one slot per SIMD
+// each; group 1 runs one phase behind, so that while one wave of a SIMD
+// issues the 16 MFMAs of a 32-wide K step from registers, the other issues
+// its DMA and reads its operands of the next step from LDS.  Every phase ends
+// with a workgroup barrier:
 //   group 0: [MEM(h) | COMP(h)] for each 32-wide step h, then one idle phase;
 //   group 1: one idle phase, then [MEM(h) | COMP(h)].
-// The ring holds S stages of BK = 32 HPS elements of K, consumed in HPS
-// steps.  With BK = 64 a K-contiguous operand row of a stage is one full
-// 128-byte line, which the global -> LDS path moves at twice the rate of
-// the 64-byte half lines of BK = 32 (only two such stages fit in LDS).
-// The first step of stage j issues the DMA of stage j + S - 1 into the
-// buffer of stage j - 1, whose last reader (group 1's MEM of stage j - 1's
-// last step) ended one barrier earlier.  Stage j + 1 must be in LDS before
-// group 0's first MEM of it: in the last step of stage j, group 0 waits for
-// its own DMA of that stage at the end of its COMP, group 1 at the end of
-// its MEM (together with its LDS reads), both before the same barrier.
-template <int T, bool RM, bool SWAP, int BK>
-__device__ inline void mainloop_pp(f32x16_t (&acc)[Tile<T>::FM][Tile<T>::FN], char* smem,
-                                   const uint16_t* a, int64_t lda, const uint16_t* b,
-                                   int64_t ldb, int K) {
-  static_assert(Tile<T>::NW == 8, "ping-pong needs two waves per SIMD");
-  using R = Ring<T, BK>;
-  constexpr int S = R::NSTAGE, PS = R::PER_STAGE, HPS = BK / 32;
-  static_assert(HPS * 32 == BK && S >= 2, "ring of 32-wide steps");
-  const int wave = threadIdx.x >> 6;
-  const int wm = wave / 4, wn = wave % 4;
-  const bool g1 = __builtin_amdgcn_readfirstlane(wave) >= 4;
-#pragma unroll
-  for (int fm = 0; fm < Tile<T>::FM; ++fm)
-#pragma unroll
-    for (int fn = 0; fn < Tile<T>::FN; ++fn)
-#pragma unroll
-      for (int v = 0; v < 16; ++v) acc[fm][fn][v] = 0.f;
-
-  const uint32_t lds0 = lds_addr(smem);
-  const int nk = K / BK;
-  auto issue = [&](int kt) {
-    const uint32_t st = lds0 + uint32_t((kt % S) * R::STAGE);
-    issue_kc<T, BK>(a, lda, kt * BK, st);
-    if constexpr (RM) issue_rm<T, BK>(b, ldb, kt * BK, st + R::A_BYTES);
-    else issue_kc<T, BK>(b, ldb, kt * BK, st + R::A_BYTES);
-  };
-  auto stage_ptr = [&](int kt) { return smem + (kt % S) * R::STAGE; };
-#pragma unroll
-  for (int s = 0; s + 1 < S; ++s)
-    if (s < nk) issue(s);
-  ring_wait<PS, S - 2>(min(nk - 1, S - 2));
-  if (g1) barrier_pinned();
-
-  Frags<T> f0, f1;
-  for (int j = 0; j < nk; ++j) {
-    const char* st = stage_ptr(j);
-    const int pend = min(nk - 1, j + S - 1) - (j + 1);
-#pragma unroll
-    for (int hs = 0; hs < HPS; ++hs) {
-      // MEM
-      if (hs == 0 && j + S - 1 < nk) issue(j + S - 1);
-      load_frags<T, RM, BK>(f0, st, st + R::A_BYTES, 2 * hs, wm, wn);
-      load_frags<T, RM, BK>(f1, st, st + R::A_BYTES, 2 * hs + 1, wm, wn);
-      if (g1) {
-        __builtin_amdgcn_s_waitcnt(0xC07F);   // lgkmcnt(0)
-        if (hs == HPS - 1) dma_wait_stages<PS>(pend);
-      }
-      barrier_pinned();
-      // COMP
-      mma<T, SWAP>(acc, f0);
-      mma<T, SWAP>(acc, f1);
-      if (!g1 && hs == HPS - 1) dma_wait_stages<PS>(pend);
-      barrier_pinned();
-    }
-  }
-  if (!g1) barrier_pinned();
-  __builtin_amdgcn_s_waitcnt(0xC07F);
-  dma_wait<0>();   // nothing is in flight here; keeps the counter model exact
-}
+// Stages are 64 K elements wide (two steps), so a K-contiguous row of a
+// stage is one full 128-byte line, which the global -> LDS path moves at
+// twice the rate of 64-byte half lines.  That path takes about 64 bytes per
+// clock and compute unit, so both loops issue one operand stage (32 KB per
+// workgroup) per step rather than a whole stage every other step.  The data
+// a step reads must be in LDS before group 0's MEM of that step: at the end
+// of the step before, group 0 waits for its own DMAs at the end of its COMP,
+// group 1 at the end of its MEM (together with its LDS reads), both before
+// the same barrier.  A buffer is refilled only after the barrier that ends
+// its last reader's MEM phase.
 
 // Ping-pong schedule of the update (operand b = the K x T row-major block of
 // Y).  A stage of b splits into two halves of BK / 2 rows without shortening
@@ -474,8 +419,8 @@ __device__ inline void mainloop_pp(f32x16_t (&acc)[Tile<T>::FM][Tile<T>::FN], ch
 // in the first step (the first step reads K rows 0 .. BK/2 - 1 of b, the
 // second the others; group 1's reads are complete at the barrier that ends
 // its memory phase, group 0's before its compute phase).  Every step ends
-// with the same wait protocol as mainloop_pp, for exactly the data the next
-// step reads; the DMAs issued after that data stay in flight:
+// with that wait protocol, for exactly the data the next step reads;
+// the DMAs issued after that data stay in flight:
 //   end of step 1 of stage j: b's second half of stage j is needed; b's
 //     first half of j + 1 and a of j + 1 (HB + DO instructions) may be pending;
 //   end of step 2: a of j + 1 and b's first half of j + 1 are needed; b's
@@ -565,6 +510,91 @@ __device__ inline void mainloop_pp_rm(f32x16_t (&acc)[Tile<T>::FM][Tile<T>::FN],
   dma_wait<0>();
 }
 
+// Ping-pong schedule of the Gram (both operands K-contiguous rows of Y).
+// Its stages cannot be split along K without halving the 128-byte row
+// pieces, so the ring holds five operand slots of one operand stage each,
+// filled in the order a(0), b(0), a(1), b(1), ...: operand stage i goes into
+// slot i % 5.  The slot of a(j + 2) is that of b(j - 1) and the slot of
+// b(j + 1) that of a(j - 1), both free once stage j - 1 has been read, so the
+// first step of stage j issues b(j + 1) and the second a(j + 2): one operand
+// stage per step.  At the end of stage j's second step every wave waits for
+// a(j + 1) and b(j + 1), leaving a(j + 2) in flight; five consecutive operand
+// stages are live at most (a(j), b(j) read, a(j + 1), b(j + 1), a(j + 2)).
+template <int T, bool SWAP, int BK>
+__device__ inline void mainloop_pp_kc5(f32x16_t (&acc)[Tile<T>::FM][Tile<T>::FN], char* smem,
+                                       const uint16_t* a, int64_t lda, const uint16_t* b,
+                                       int64_t ldb, int K) {
+  static_assert(Tile<T>::NW == 8, "ping-pong needs two waves per SIMD");
+  using R = Ring<T, BK>;
+  constexpr int DO = R::DMA_OP, SLOTS = 5;
+  static_assert(BK == 64, "two 32-wide steps per stage");
+  static_assert(SLOTS * R::A_BYTES <= R::LDS, "five operand slots");
+  const int wave = threadIdx.x >> 6;
+  const int wm = wave / 4, wn = wave % 4;
+  const bool g1 = __builtin_amdgcn_readfirstlane(wave) >= 4;
+#pragma unroll
+  for (int fm = 0; fm < Tile<T>::FM; ++fm)
+#pragma unroll
+    for (int fn = 0; fn < Tile<T>::FN; ++fn)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) acc[fm][fn][v] = 0.f;
+
+  const uint32_t lds0 = lds_addr(smem);
+  const int nk = K / BK;
+  auto slot_lds = [&](int i) { return lds0 + uint32_t((i % SLOTS) * R::A_BYTES); };
+  auto slot_ptr = [&](int i) { return smem + (i % SLOTS) * R::A_BYTES; };
+  auto issue_a = [&](int kt) { issue_kc<T, BK>(a, lda, kt * BK, slot_lds(2 * kt)); };
+  auto issue_b = [&](int kt) { issue_kc<T, BK>(b, ldb, kt * BK, slot_lds(2 * kt + 1)); };
+
+  issue_a(0);
+  issue_b(0);
+  if (nk > 1) {
+    issue_a(1);
+    __builtin_amdgcn_s_waitcnt(0xC07F);
+    ring_sync_dma<DO>();
+  } else {
+    __builtin_amdgcn_s_waitcnt(0xC07F);
+    ring_sync_dma<0>();
+  }
+  if (g1) barrier_pinned();
+
+  Frags<T> f0, f1;
+  for (int j = 0; j < nk; ++j) {
+    const char* sa = slot_ptr(2 * j);
+    const char* sb = slot_ptr(2 * j + 1);
+#pragma unroll
+    for (int hs = 0; hs < 2; ++hs) {
+      // MEM
+      if (hs == 0) {
+        if (j + 1 < nk) issue_b(j + 1);
+      } else {
+        if (j + 2 < nk) issue_a(j + 2);
+      }
+      load_frags<T, false, BK>(f0, sa, sb, 2 * hs, wm, wn);
+      load_frags<T, false, BK>(f1, sa, sb, 2 * hs + 1, wm, wn);
+      if (g1) {
+        __builtin_amdgcn_s_waitcnt(0xC07F);   // lgkmcnt(0)
+        if (hs == 1) {
+          if (j + 2 < nk) dma_wait<DO>();
+          else dma_wait<0>();
+        }
+      }
+      barrier_pinned();
+      // COMP
+      mma<T, SWAP>(acc, f0);
+      mma<T, SWAP>(acc, f1);
+      if (!g1 && hs == 1) {
+        if (j + 2 < nk) dma_wait<DO>();
+        else dma_wait<0>();
+      }
+      barrier_pinned();
+    }
+  }
+  if (!g1) barrier_pinned();
+  __builtin_amdgcn_s_waitcnt(0xC07F);
+  dma_wait<0>();
+}
+
 template <int T, bool RM, bool SWAP, int BK>
 __device__ inline void run_mainloop(f32x16_t (&acc)[Tile<T>::FM][Tile<T>::FN], char* smem,
                                     const uint16_t* a, int64_t lda, const uint16_t* b,
@@ -572,7 +602,7 @@ __device__ inline void run_mainloop(f32x16_t (&acc)[Tile<T>::FM][Tile<T>::FN], c
   if constexpr (Tile<T>::NW == 8 && RM) {
     mainloop_pp_rm<T, SWAP, BK>(acc, smem, a, lda, b, ldb, K);
   } else if constexpr (Tile<T>::NW == 8) {
-    mainloop_pp<T, RM, SWAP, BK>(acc, smem, a, lda, b, ldb, K);
+    mainloop_pp_kc5<T, SWAP, BK>(acc, smem, a, lda, b, ldb, K);
   } else {
     mainloop<T, RM, SWAP, BK>(acc, smem, a, lda, b, ldb, K);
   }
