@@ -24,16 +24,15 @@
 // 128 x 64 blocks; smaller tiles run 4 waves in a 2 x 2 grid.  Each wave
 // accumulates 32 x 32 v_mfma_f32_32x32x16_bf16 blocks.  Operands reach LDS
 // through global_load_lds_dwordx4 (direct to LDS, no VGPR staging) into a
-// ring of stages: two of 64 K elements for the 256 tile (five operand slots
-// of 64 K elements for its Gram), three or four of 32, 64 or 128 for the
-// smaller ones.  K-contiguous
-// operands are stored as rows of 2 BK bytes whose 16-byte chunks are
-// XOR-swizzled by row group; the update's Y operand (and on the 256 tile the
-// polynomial's second A operand) is staged in its row-major layout (BK rows
+// ring of stages: two of 64 K elements for the 256 tile's update, five
+// operand slots of 64 K elements for its Gram and polynomial, three or four
+// stages of 32, 64 or 128 for the smaller tiles.  K-contiguous operands are
+// stored as rows of 2 BK bytes whose 16-byte chunks are XOR-swizzled by row
+// group; the update's Y operand is staged in its row-major layout (BK rows
 // of T bf16) with 32-byte chunks XOR-swizzled per row and read with
 // ds_read_b64_tr_b16, which hands each lane 4 consecutive K values of one
-// column.  Both layouts are free of LDS bank conflicts for
-// the reads.
+// column.  Both layouts are free of LDS bank conflicts for the main-loop
+// reads.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -76,7 +75,8 @@ struct Ring {
   static constexpr int RPB = 256 / RB;
   static constexpr int A_BYTES = T * RB;         // one operand stage
   static constexpr int STAGE = 2 * A_BYTES;
-  // the 256 tile's Gram keeps five operand slots of A_BYTES (mainloop_pp_kc5)
+  // the 256 tile's Gram and polynomial keep five operand slots of A_BYTES
+  // (mainloop_pp_kc5)
   static constexpr int LDS = T == 256 ? 5 * A_BYTES : NSTAGE * STAGE;
   static constexpr int DMA_OP = T * BK / 512 / Tile<T>::NW;   // 1 KB DMAs per wave per operand
   static constexpr int PER_STAGE = 2 * DMA_OP;
@@ -510,11 +510,11 @@ __device__ inline void mainloop_pp_rm(f32x16_t (&acc)[Tile<T>::FM][Tile<T>::FN],
   dma_wait<0>();
 }
 
-// Ping-pong schedule of the Gram (both operands K-contiguous rows of Y).
-// Its stages cannot be split along K without halving the 128-byte row
-// pieces, so the ring holds five operand slots of one operand stage each,
-// filled in the order a(0), b(0), a(1), b(1), ...: operand stage i goes into
-// slot i % 5.  The slot of a(j + 2) is that of b(j - 1) and the slot of
+// Ping-pong schedule of the Gram and the polynomial (both operands
+// K-contiguous rows, of Y or of A).  Their stages cannot be split along K
+// without halving the 128-byte row pieces, so the ring holds five operand
+// slots of one operand stage each, filled in the order a(0), b(0), a(1),
+// b(1), ...: operand stage i goes into slot i % 5.  The slot of a(j + 2) is that of b(j - 1) and the slot of
 // b(j + 1) that of a(j - 1), both free once stage j - 1 has been read, so the
 // first step of stage j issues b(j + 1) and the second a(j + 2): one operand
 // stage per step.  At the end of stage j's second step every wave waits for
@@ -1040,14 +1040,7 @@ __global__ __launch_bounds__(Tile<T>::NT) void k_poly_fast(const Phase P) {
   uint16_t* B = reinterpret_cast<uint16_t*>(w + WL.b);
   const int64_t ldg = WL.ldg;
   f32x16_t acc[FM][FN];
-  // A is stored exactly symmetric (mirrored stores of the same values), so
-  // the K x T row-major block of its columns J holds the rows J: the 8-wave
-  // tile reads that operand row-major, which lets its ping-pong spread the
-  // DMA over both steps of a stage.  The MFMA operands are the same values.
-  if constexpr (Tile<T>::NW == 8)
-    run_mainloop<T, true, false, BK>(acc, smem, A + int64_t(I) * T * ldg, ldg, A + int64_t(J) * T, ldg, kp);
-  else
-    run_mainloop<T, false, false, BK>(acc, smem, A + int64_t(I) * T * ldg, ldg, A + int64_t(J) * T * ldg, ldg, kp);
+  run_mainloop<T, false, false, BK>(acc, smem, A + int64_t(I) * T * ldg, ldg, A + int64_t(J) * T * ldg, ldg, kp);
   load_rows<T>(smem, A, ldg, int64_t(J) * T, int64_t(I) * T);
   __syncthreads();
   const float a = P.a, b = P.b, c = P.c;
