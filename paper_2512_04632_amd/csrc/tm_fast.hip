@@ -407,7 +407,10 @@ __device__ inline void mainloop(f32x16_t (&acc)[Tile<T>::FM][Tile<T>::FN], char*
 // of the step before, group 0 waits for its own DMAs at the end of its COMP,
 // group 1 at the end of its MEM (together with its LDS reads), both before
 // the same barrier.  A buffer is refilled only after the barrier that ends
-// its last reader's MEM phase.
+// its last reader's MEM phase.  A MEM phase issues its LDS reads before its
+// DMA: issuing a DMA stalls the wave while the compute unit's queue drains,
+// and that stall then overlaps the reads' completion instead of delaying
+// their start.
 
 // Ping-pong schedule of the update (operand b = the K x T row-major block of
 // Y).  A stage of b splits into two halves of BK / 2 rows without shortening
@@ -485,14 +488,14 @@ __device__ inline void mainloop_pp_rm(f32x16_t (&acc)[Tile<T>::FM][Tile<T>::FN],
 #pragma unroll
     for (int hs = 0; hs < 2; ++hs) {
       // MEM
+      load_frags<T, true, BK>(f0, st, st + R::A_BYTES, 2 * hs, wm, wn);
+      load_frags<T, true, BK>(f1, st, st + R::A_BYTES, 2 * hs + 1, wm, wn);
       if (hs == 0) {
         if (j + 1 < nk) issue_a(j + 1);
       } else {
         if (j + 1 < nk) issue_b(j + 1, 1);
         if (j + 2 < nk) issue_b(j + 2, 0);
       }
-      load_frags<T, true, BK>(f0, st, st + R::A_BYTES, 2 * hs, wm, wn);
-      load_frags<T, true, BK>(f1, st, st + R::A_BYTES, 2 * hs + 1, wm, wn);
       if (g1) {
         __builtin_amdgcn_s_waitcnt(0xC07F);   // lgkmcnt(0)
         wait_step(j, hs);
@@ -565,13 +568,13 @@ __device__ inline void mainloop_pp_kc5(f32x16_t (&acc)[Tile<T>::FM][Tile<T>::FN]
 #pragma unroll
     for (int hs = 0; hs < 2; ++hs) {
       // MEM
+      load_frags<T, false, BK>(f0, sa, sb, 2 * hs, wm, wn);
+      load_frags<T, false, BK>(f1, sa, sb, 2 * hs + 1, wm, wn);
       if (hs == 0) {
         if (j + 1 < nk) issue_b(j + 1);
       } else {
         if (j + 2 < nk) issue_a(j + 2);
       }
-      load_frags<T, false, BK>(f0, sa, sb, 2 * hs, wm, wn);
-      load_frags<T, false, BK>(f1, sa, sb, 2 * hs + 1, wm, wn);
       if (g1) {
         __builtin_amdgcn_s_waitcnt(0xC07F);   // lgkmcnt(0)
         if (hs == 1) {
