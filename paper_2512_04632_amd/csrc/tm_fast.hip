@@ -51,11 +51,18 @@ typedef short s16x4_t __attribute__((ext_vector_type(4)));
 // Tile T x T computed by NW wave64s in a WGM x WGN grid (2 x 4, 2 x 2, or a
 // single wave for the 32 tile); each wave owns TWM x TWN of the output as
 // 32 x 32 MFMA blocks.
+// The smaller tiles' Gram and polynomial add NP producer waves that only
+// issue the ring's DMA (mainloop_pc); they leave after the main loop, so the
+// epilogues run on the NT threads of the NW compute waves.  (The update's
+// smaller tiles keep the DMA in their compute waves: producer waves made
+// them slower.)
 template <int T>
 struct Tile {
   static constexpr int NW = T == 256 ? 8 : (T == 32 ? 1 : 4);   // 2 waves per SIMD for 256
   static constexpr int WGM = NW == 1 ? 1 : 2, WGN = NW / WGM;
-  static constexpr int NT = 64 * NW;            // threads per workgroup
+  static constexpr int NT = 64 * NW;            // threads of the compute waves
+  static constexpr int NP = T == 256 ? 0 : (T == 32 ? 1 : 2);   // producer waves
+  static constexpr int NTT = 64 * (NW + NP);    // threads per workgroup
   static constexpr int TWM = T / WGM, TWN = T / WGN;
   static constexpr int FM = TWM / 32, FN = TWN / 32;
 };
@@ -167,6 +174,19 @@ __device__ inline void dma_wait() {
   else static_assert(PENDING == 0, "unsupported in-flight count");
 }
 
+// DMA-only wait for all but `stages` stages of PS instructions (stages <= MAXS).
+template <int PS, int MAXS>
+__device__ inline void dma_wait_upto(int stages) {
+  static_assert(MAXS * PS <= 63, "in-flight count beyond vmcnt");
+  if constexpr (MAXS >= 2) {
+    if (stages >= 2) { dma_wait<2 * PS>(); return; }
+  }
+  if constexpr (MAXS >= 1) {
+    if (stages == 1) { dma_wait<PS>(); return; }
+  }
+  dma_wait<0>();
+}
+
 template <int PS>
 __device__ inline void dma_wait_stages(int stages) {
   if (stages >= 3) dma_wait<3 * PS>();
@@ -195,6 +215,20 @@ __device__ inline void dma_kc(const uint16_t* src, int64_t ld, int k0, uint32_t 
   constexpr int RPI = 64 / R::CPR;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int j = wave + Tile<T>::NW * q;
+  const int r = j * RPI + lane / R::CPR;
+  const int c = (lane % R::CPR) ^ ((r / R::RPB) % R::CPR);
+  const uint32_t voff = uint32_t((int64_t(r) * ld + k0 + c * 8) * 2);
+  dma16(src, voff, __builtin_amdgcn_readfirstlane(lds + uint32_t(j) * 1024u));
+}
+
+// The same 1 KB instructions split over NI issuing waves (w = 0 .. NI - 1):
+// instruction q of wave w fills 1 KB block w + NI q of the operand stage.
+template <int T, int BK, int NI>
+__device__ inline void dma_kc_w(const uint16_t* src, int64_t ld, int k0, uint32_t lds, int q, int w) {
+  using R = Ring<T, BK>;
+  constexpr int RPI = 64 / R::CPR;
+  const int lane = threadIdx.x & 63;
+  const int j = w + NI * q;
   const int r = j * RPI + lane / R::CPR;
   const int c = (lane % R::CPR) ^ ((r / R::RPB) % R::CPR);
   const uint32_t voff = uint32_t((int64_t(r) * ld + k0 + c * 8) * 2);
@@ -305,9 +339,10 @@ __device__ inline void mma(f32x16_t (&acc)[Tile<T>::FM][Tile<T>::FN], const Frag
     }
 }
 
-// 4-wave main loop.  acc = A (T x K, K-contiguous rows of a) * B^T where B's
-// rows are the K-contiguous rows of b (RM = false) or B = the K x T row-major
-// block of b (RM = true); K is a multiple of BK and every tile is full.  The
+// 4-wave main loop of the update's 128 and 64 tiles.  acc = A (T x K,
+// K-contiguous rows of a) * B^T where B's rows are the K-contiguous rows of b
+// (RM = false) or B = the K x T row-major block of b (RM = true); K is a
+// multiple of BK and every tile is full.  The
 // operands of each 16-wide K slice are read from LDS while the previous
 // slice's MFMAs run.  The DMA is spread over the K slices: while stage kt is
 // read and multiplied, each wave issues its share of stage kt + NSTAGE - 1,
@@ -388,6 +423,90 @@ __device__ inline void mainloop(f32x16_t (&acc)[Tile<T>::FM][Tile<T>::FN], char*
     }
   }
   ring_sync<0>();   // the ring is free for the epilogue
+}
+
+// Producer/consumer main loop of the smaller tiles' Gram and polynomial
+// (both operands K-contiguous).  With one compute wave
+// per SIMD, the stall of a DMA issue (the wave waits while the compute
+// unit's global -> LDS queue drains) left the SIMD's matrix core idle, so
+// NP extra waves issue the whole ring's DMA while the NW compute waves only
+// read LDS and multiply.  Per stage kt, between two workgroup barriers: the
+// producers issue stage kt + NST - 1 into the buffer of stage kt - 1 (read
+// before the last barrier) and wait for their DMA of stage kt + 1; the
+// compute waves multiply stage kt, loading the operands of each 16-wide
+// slice while the previous slice's MFMAs run, and finish their LDS reads
+// before the barrier.  Slices are consumed in increasing K order, so every
+// output element accumulates the same products in the same order as in the
+// other loops.  The producer waves return afterwards; a barrier then waits
+// only for the waves still running.
+template <int T, bool SWAP, int BK>
+__device__ inline bool mainloop_pc(f32x16_t (&acc)[Tile<T>::FM][Tile<T>::FN], char* smem,
+                                   const uint16_t* a, int64_t lda, const uint16_t* b,
+                                   int64_t ldb, int K) {
+  using R = Ring<T, BK>;
+  constexpr int NW = Tile<T>::NW, NP = Tile<T>::NP, NS = BK / 16, NST = R::NSTAGE;
+  constexpr int DOP = T * BK / 512 / NP;     // 1 KB DMAs per producer and operand stage
+  constexpr int PSP = 2 * DOP;
+  static_assert(NP >= 1 && DOP * NP * 512 == T * BK, "whole DMA instructions per producer");
+  static_assert(NS % 2 == 0, "slices in pairs");
+  const int wave = __builtin_amdgcn_readfirstlane(int(threadIdx.x >> 6));
+  const bool prod = wave >= NW;
+  const uint32_t lds0 = lds_addr(smem);
+  const int nk = K / BK;
+  auto stage_ptr = [&](int kt) { return smem + (kt % NST) * R::STAGE; };
+  if (prod) {
+    const int pw = wave - NW;
+    auto issue = [&](int kt) {
+      const uint32_t st = lds0 + uint32_t((kt % NST) * R::STAGE);
+#pragma unroll
+      for (int q = 0; q < DOP; ++q) dma_kc_w<T, BK, NP>(a, lda, kt * BK, st, q, pw);
+#pragma unroll
+      for (int q = 0; q < DOP; ++q) dma_kc_w<T, BK, NP>(b, ldb, kt * BK, st + R::A_BYTES, q, pw);
+    };
+    for (int s = 0; s + 1 < NST && s < nk; ++s) issue(s);
+    dma_wait_upto<PSP, NST - 2>(min(nk - 1, NST - 2));
+    barrier_pinned();
+    for (int kt = 0; kt < nk; ++kt) {
+      if (kt + NST - 1 < nk) issue(kt + NST - 1);
+      dma_wait_upto<PSP, NST - 2>(min(nk - 1, kt + NST - 1) - (kt + 1));
+      barrier_pinned();
+    }
+    dma_wait<0>();
+    return false;
+  }
+  const int wm = wave / Tile<T>::WGN, wn = wave % Tile<T>::WGN;
+#pragma unroll
+  for (int fm = 0; fm < Tile<T>::FM; ++fm)
+#pragma unroll
+    for (int fn = 0; fn < Tile<T>::FN; ++fn)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) acc[fm][fn][v] = 0.f;
+  barrier_pinned();   // stage 0 has landed
+  Frags<T> f0, f1;
+  load_frags<T, false, BK>(f0, stage_ptr(0), stage_ptr(0) + R::A_BYTES, 0, wm, wn);
+  for (int kt = 0; kt < nk; ++kt) {
+    const char* st = stage_ptr(kt);
+#pragma unroll
+    for (int s = 0; s < NS; s += 2) {
+      load_frags<T, false, BK>(f1, st, st + R::A_BYTES, s + 1, wm, wn);
+      mma<T, SWAP>(acc, f0);
+      if (s + 2 < NS) {
+        load_frags<T, false, BK>(f0, st, st + R::A_BYTES, s + 2, wm, wn);
+        mma<T, SWAP>(acc, f1);
+      } else {
+        __builtin_amdgcn_sched_barrier(0);
+        __builtin_amdgcn_s_waitcnt(0xC07F);   // lgkmcnt(0): stage kt is read
+        barrier_pinned();                     // and stage kt + 1 has landed
+        if (kt + 1 < nk) {
+          const char* nxp = stage_ptr(kt + 1);
+          load_frags<T, false, BK>(f0, nxp, nxp + R::A_BYTES, 0, wm, wn);
+        }
+        __builtin_amdgcn_sched_barrier(0);
+        mma<T, SWAP>(acc, f1);
+      }
+    }
+  }
+  return true;
 }
 
 // Ping-pong schedule of the 8-wave tile (two loops below, one per layout of
@@ -599,15 +718,21 @@ __device__ inline void mainloop_pp_kc5(f32x16_t (&acc)[Tile<T>::FM][Tile<T>::FN]
 }
 
 template <int T, bool RM, bool SWAP, int BK>
-__device__ inline void run_mainloop(f32x16_t (&acc)[Tile<T>::FM][Tile<T>::FN], char* smem,
+// Returns false in the producer waves, which then leave the kernel.
+__device__ inline bool run_mainloop(f32x16_t (&acc)[Tile<T>::FM][Tile<T>::FN], char* smem,
                                     const uint16_t* a, int64_t lda, const uint16_t* b,
                                     int64_t ldb, int K) {
   if constexpr (Tile<T>::NW == 8 && RM) {
     mainloop_pp_rm<T, SWAP, BK>(acc, smem, a, lda, b, ldb, K);
+    return true;
   } else if constexpr (Tile<T>::NW == 8) {
     mainloop_pp_kc5<T, SWAP, BK>(acc, smem, a, lda, b, ldb, K);
-  } else {
+    return true;
+  } else if constexpr (RM) {   // the update's smaller tiles: compute waves issue the DMA
     mainloop<T, RM, SWAP, BK>(acc, smem, a, lda, b, ldb, K);
+    return true;
+  } else {
+    return mainloop_pc<T, SWAP, BK>(acc, smem, a, lda, b, ldb, K);
   }
 }
 
@@ -948,7 +1073,7 @@ __device__ inline void store_sym_f32(const f32x16_t (&acc)[Tile<T>::FM][Tile<T>:
 
 // ---------------------------------------------------------------- kernels
 template <int T, int BK>
-__global__ __launch_bounds__(Tile<T>::NT) void k_gram_fast(const Phase P) {
+__global__ __launch_bounds__(Tile<T>::NTT) void k_gram_fast(const Phase P) {
   __shared__ __attribute__((aligned(1024))) char smem[smem_bytes<T, BK>()];
   constexpr int FM = Tile<T>::FM, FN = Tile<T>::FN;
   Loc L;
@@ -961,7 +1086,7 @@ __global__ __launch_bounds__(Tile<T>::NT) void k_gram_fast(const Phase P) {
   const WsLayout WL = ws_layout(E.kp, E.Np, 2);
   const int64_t ldy = WL.ldy;
   f32x16_t acc[FM][FN];
-  run_mainloop<T, false, false, BK>(acc, smem, Y + int64_t(I) * T * ldy, ldy, Y + int64_t(J) * T * ldy, ldy, Np);
+  if (!run_mainloop<T, false, false, BK>(acc, smem, Y + int64_t(I) * T * ldy, ldy, Y + int64_t(J) * T * ldy, ldy, Np)) return;
 
   if (P.flags & kA32) {
     store_sym_f32<T>(acc, reinterpret_cast<float*>(w + WL.a32), kp, I, J);
@@ -1029,7 +1154,7 @@ __global__ __launch_bounds__(Tile<T>::NT) void k_gram_fast(const Phase P) {
 // B~ = b A + c A A + a I (upper tiles, mirrored).  The stage is preloaded with
 // A's tile (J, I), whose element (j, i) equals A_ij.
 template <int T, int BK, bool SCALED>
-__global__ __launch_bounds__(Tile<T>::NT) void k_poly_fast(const Phase P) {
+__global__ __launch_bounds__(Tile<T>::NTT) void k_poly_fast(const Phase P) {
   __shared__ __attribute__((aligned(1024))) char smem[smem_bytes<T, BK>()];
   constexpr int FM = Tile<T>::FM, FN = Tile<T>::FN;
   Loc L;
@@ -1043,7 +1168,7 @@ __global__ __launch_bounds__(Tile<T>::NT) void k_poly_fast(const Phase P) {
   uint16_t* B = reinterpret_cast<uint16_t*>(w + WL.b);
   const int64_t ldg = WL.ldg;
   f32x16_t acc[FM][FN];
-  run_mainloop<T, false, false, BK>(acc, smem, A + int64_t(I) * T * ldg, ldg, A + int64_t(J) * T * ldg, ldg, kp);
+  if (!run_mainloop<T, false, false, BK>(acc, smem, A + int64_t(I) * T * ldg, ldg, A + int64_t(J) * T * ldg, ldg, kp)) return;
   load_rows<T>(smem, A, ldg, int64_t(J) * T, int64_t(I) * T);
   __syncthreads();
   const float a = P.a, b = P.b, c = P.c;
@@ -1188,7 +1313,7 @@ __global__ __launch_bounds__(256) void k_apply_s(const Phase P) {
 }
 
 #define TM_LAUNCH(kern) \
-  do { hipLaunchKernelGGL(kern, dim3(P.total), dim3(Tile<T>::NT), 0, st, P); return hipGetLastError(); } while (0)
+  do { hipLaunchKernelGGL(kern, dim3(P.total), dim3(Tile<T>::NTT), 0, st, P); return hipGetLastError(); } while (0)
 
 template <int T, int BK>
 static hipError_t launch_t(int kind, const Phase& P, hipStream_t st) {
@@ -1198,7 +1323,10 @@ static hipError_t launch_t(int kind, const Phase& P, hipStream_t st) {
       if (P.flags & kScale) TM_LAUNCH((k_poly_fast<T, BK, true>));
       TM_LAUNCH((k_poly_fast<T, BK, false>));
     case kKindUpdate:
-      if constexpr (T >= 64) TM_LAUNCH((k_update_fast<T, BK>));   // layout tiles only
+      if constexpr (T >= 64) {   // layout tiles only; no producer waves
+        hipLaunchKernelGGL((k_update_fast<T, BK>), dim3(P.total), dim3(Tile<T>::NT), 0, st, P);
+        return hipGetLastError();
+      }
       break;
   }
   return hipErrorInvalidValue;
