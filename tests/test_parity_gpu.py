@@ -151,6 +151,29 @@ def test_batched_grouped_single_are_bitwise_equal(m, n, dtype):
     assert np.array_equal(again, single[0])        # run-to-run determinism
 
 
+# ----------------------------------------------------------------- one-stage main loops
+@pytest.mark.parametrize("m,n", [(64, 64), (40, 56)])
+def test_many_small_matrices_one_stage_loops(m, n):
+    """300 matrices padded to 64 x 64: the batched call's first Gram and its updates
+    run more than 256 tiles of 64, so their ring stages are 64 wide and K = 64 is a
+    single stage (the producer-wave loop and the update loop with one stage); the
+    grouped call splits them over launches of 64 matrices, with other stage widths.
+    Both must agree bit for bit with single calls and stay within the oracle's
+    tolerance."""
+    log(f"case: batch of 300 {m}x{n} bf16 AOL t=4")
+    Xs = [make_input(m, n, 0.8, 1000 + s, "bf16") for s in range(300)]
+    tb = torch.stack([to_device(X, "bf16") for X in Xs]).contiguous()
+    tm.orthogonalize(tb, 4, None, "aol")
+    tg = [to_device(X, "bf16") for X in Xs]
+    tm.orthogonalize_grouped(tg, 4, None, "aol")
+    torch.cuda.synchronize()
+    for i in range(0, 300, 37):
+        G = from_device(tb[i])
+        assert np.array_equal(from_device(tg[i]), G), i
+        assert np.array_equal(gpu_orth(Xs[i], "bf16", 4, "aol"), G), i
+        assert relF(G, O.orthogonalize(Xs[i], 4)) <= BF16_TOL, i
+
+
 # ----------------------------------------------------------------- grouped workloads
 def run_workload(name, iters=4, precond="aol"):
     shapes = synth.workload_shapes(name)
