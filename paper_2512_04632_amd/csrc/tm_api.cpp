@@ -439,6 +439,14 @@ tm_status plan_f32(const Plan& pl, int iters, const float* coeffs, int precond) 
 tm_status run_locked(std::vector<Item>& items, int esz, int iters, const float* coeffs,
                      int precond, hipStream_t st, int dev) {
   tm_status s = TM_OK;
+  // A call of more than kMaxEntries items runs every phase as several
+  // launches; largest products first, so the last, partly filled launch
+  // holds the shortest tiles.  Each matrix's arithmetic does not depend on
+  // the launch it lands in.
+  if (items.size() > size_t(tmk::kMaxEntries))
+    std::stable_sort(items.begin(), items.end(), [](const Item& x, const Item& y) {
+      return double(x.k) * x.k * x.N * x.count > double(y.k) * y.k * y.N * y.count;
+    });
   int tcfg = 0;
   if (esz == 2) {
     tcfg = choose_tile_cfg(items);
