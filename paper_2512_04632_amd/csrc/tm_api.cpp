@@ -255,12 +255,22 @@ tm_status launch(const Plan& pl, int kind, int cfg, int src, int dst, float a, f
     Phase P;
     std::memset(&P, 0, sizeof(P));
     const size_t n = std::min(items.size() - base, size_t(tmk::kMaxEntries));
+    // update launches take their largest products first (the longest tiles
+    // start first); every entry carries its own workspace offset
+    std::vector<size_t> idx(n);
+    for (size_t i = 0; i < n; ++i) idx[i] = base + i;
+    if (kind == tmk::kKindUpdate)
+      std::stable_sort(idx.begin(), idx.end(), [&](size_t x, size_t y) {
+        const Item& u = items[x];
+        const Item& v = items[y];
+        return double(u.k) * u.k * u.N * u.count > double(v.k) * v.k * v.N * v.count;
+      });
     uint64_t start = 0;
     for (size_t i = 0; i < n; ++i) {
-      const Item& it = items[base + i];
+      const Item& it = items[idx[i]];
       Entry& E = P.e[i];
       E.x = it.x;
-      E.ws = pl.ws_off[base + i];
+      E.ws = pl.ws_off[idx[i]];
       E.k = it.k;
       E.N = it.N;
       E.kp = it.kp;
