@@ -198,7 +198,20 @@ struct Plan {
   char* ws;
   int esz;
   hipStream_t st;
+  int tcfg = 0;                   // bf16: the call's layout tile
 };
+
+// bf16 update of one launch of a call split over several launches: the
+// largest tile (at most the layout tile) with about two waves of tiles.
+int choose_update_cfg(int tcfg, const std::vector<Item>& items) {
+  for (int cfg = tcfg; cfg < tmk::kNumCfg - 1; ++cfg) {
+    uint64_t tiles = 0;
+    for (const Item& it : items)
+      tiles += uint64_t(it.count) * tmk::blocks_per_matrix(tmk::kKindUpdate, cfg, it.k, it.N, it.kp, it.Np);
+    if (tiles >= 480) return cfg;
+  }
+  return tmk::kNumCfg - 1;
+}
 
 // Compute units of the MI355X: the blocks of one full wave of the large tiles.
 constexpr int kWave = 256;
@@ -265,6 +278,18 @@ tm_status launch(const Plan& pl, int kind, int cfg, int src, int dst, float a, f
         const Item& v = items[y];
         return double(u.k) * u.k * u.N * u.count > double(v.k) * v.k * v.N * v.count;
       });
+    // a call split over several launches picks each launch's tile for that
+    // launch's matrices (the last one may be much smaller); a product's
+    // arithmetic does not depend on the tile size
+    int ccfg = cfg;
+    if (pl.esz == 2 && items.size() > size_t(tmk::kMaxEntries) &&
+        (kind == tmk::kKindGram || kind == tmk::kKindPoly || kind == tmk::kKindUpdate)) {
+      std::vector<Item> chunk;
+      for (size_t i = 0; i < n; ++i) chunk.push_back(items[idx[i]]);
+      ccfg = kind == tmk::kKindUpdate
+                 ? choose_update_cfg(pl.tcfg, chunk)
+                 : choose_sym_cfg(kind, pl.tcfg, chunk, kind == tmk::kKindPoly || flags == 0u);
+    }
     uint64_t start = 0;
     for (size_t i = 0; i < n; ++i) {
       const Item& it = items[idx[i]];
@@ -279,7 +304,7 @@ tm_status launch(const Plan& pl, int kind, int cfg, int src, int dst, float a, f
       E.flags = (it.tall ? tmk::kTall : 0u) | (it.direct ? tmk::kDirect : 0u);
       E.tile_start = uint32_t(start);
       const bool skip = (cover == kCoverTall && !it.tall) || (cover == kCoverCopied && it.direct);
-      E.tiles_per = skip ? 0u : tmk::blocks_per_matrix(kind, cfg, it.k, it.N, it.kp, it.Np);
+      E.tiles_per = skip ? 0u : tmk::blocks_per_matrix(kind, ccfg, it.k, it.N, it.kp, it.Np);
       start += uint64_t(E.tiles_per) * it.count;
     }
     if (start >= (uint64_t(1) << 31))
@@ -301,19 +326,19 @@ tm_status launch(const Plan& pl, int kind, int cfg, int src, int dst, float a, f
     // 2 x 2 sub-tiles of 128 x 128 in a second launch that fits in one wave
     // (same per-element arithmetic, four times the blocks for the idle units).
     const bool mc = kind == tmk::kKindGram || kind == tmk::kKindPoly || kind == tmk::kKindUpdate;
-    const int tail = (pl.esz == 2 && cfg == 0 && mc && P.total > kWave && P.total % kWave <= kWave / 4)
+    const int tail = (pl.esz == 2 && ccfg == 0 && mc && P.total > kWave && P.total % kWave <= kWave / 4)
                          ? P.total % kWave
                          : 0;
     if (tail > 0) {
       P.total -= tail;
-      s = fire(pl, kind, cfg, P);
+      s = fire(pl, kind, ccfg, P);
       Phase Q = P;
       Q.flags |= tmk::kTail;
       Q.tail_base = P.total;
       Q.total = 4 * tail;
       if (s == TM_OK) s = fire(pl, kind, 1, Q);
     } else {
-      s = fire(pl, kind, cfg, P);
+      s = fire(pl, kind, ccfg, P);
     }
     if (s != TM_OK) return s;
   }
@@ -475,6 +500,7 @@ tm_status run_locked(std::vector<Item>& items, int esz, int iters, const float* 
   pl.items = &items;
   pl.esz = esz;
   pl.st = st;
+  pl.tcfg = tcfg;
   uint64_t total = 0;
   for (const Item& it : items) {
     pl.ws_off.push_back(total);
