@@ -11,7 +11,8 @@
 //                 the fp32 accumulators are stored instead (A0 is rescaled
 //                 before rounding) and the epilogue emits the AOL row sums
 //                 sum_j |A0_ij| (eq. (aol))
-//   k_apply_s     A1 = diag(s) A0 diag(s), rounded once to bf16
+//   k_apply_s     A1 = diag(s) A0 diag(s), rounded once to bf16, from the
+//                 upper tiles of A0
 //   k_poly_fast   B~ = b A + c A A + a I, upper tiles, mirrored store; at
 //                 iteration 1 it stores C = B~ diag(s) instead, so that X1 =
 //                 diag(s) X0 is never formed: B~ X1 = C X0
@@ -21,7 +22,8 @@
 //
 // Main loop: the 256 x 256 tile runs 8 wave64s (two per SIMD, so one wave's
 // barrier or DMA issue can hide behind the other's MFMAs) in a 2 x 4 grid of
-// 128 x 64 blocks; smaller tiles run 4 waves in a 2 x 2 grid.  Each wave
+// 128 x 64 blocks; smaller tiles run 4 compute waves in a 2 x 2 grid (the 32
+// tile one), plus producer waves for the Gram and polynomial.  Each wave
 // accumulates 32 x 32 v_mfma_f32_32x32x16_bf16 blocks.  Operands reach LDS
 // through global_load_lds_dwordx4 (direct to LDS, no VGPR staging) into a
 // ring of stages: two of 64 K elements for the 256 tile's update, five
@@ -1046,8 +1048,8 @@ __device__ inline void epilogue_sym_scaled(const f32x16_t (&acc)[Tile<T>::FM][Ti
   store_cols<T>(st, D, ld, int64_t(I) * T, int64_t(J) * T);   // C[i][j]
 }
 
-// fp32 store of a symmetric tile and its mirror straight from the registers
-// (first Gram only).
+// fp32 store of an upper tile straight from the registers (first Gram only;
+// k_apply_s reads the upper tiles and writes both halves of A1).
 template <int T>
 __device__ inline void store_sym_f32(const f32x16_t (&acc)[Tile<T>::FM][Tile<T>::FN], float* D,
                                      int64_t ld, int I, int J) {
@@ -1066,7 +1068,6 @@ __device__ inline void store_sym_f32(const f32x16_t (&acc)[Tile<T>::FM][Tile<T>:
           m[u] = acc[fm][fn][4 * v4 + u];
           D[int64_t(ib + u) * ld + j] = m[u];
         }
-        if (I != J) *reinterpret_cast<float4*>(D + int64_t(j) * ld + ib) = *reinterpret_cast<const float4*>(m);
       }
     }
 }
@@ -1290,26 +1291,51 @@ __global__ __launch_bounds__(256) void k_load_in(const Phase P) {
   }
 }
 
-// First iteration after AOL / Frobenius scaling: A1 = bf16(s_i A0_ij s_j)
-// over the padded kp x kp square and X1 = bf16(s_i X0_il) in place on slot 0;
-// 8 elements per thread, the A blocks first.
+// First iteration after the scaling: A1 = bf16(s_i A0_ij s_j).  The Gram
+// stored A0 (fp32) as its upper tiles only, which contain every upper 64 x 64
+// tile whatever its tile size; one block per upper 64 x 64 tile (I <= J)
+// reads it once and writes A1's tile (I, J) and, off the diagonal, its
+// transpose (J, I) through LDS (s_i s_j = s_j s_i, so the mirror holds the
+// same values).  Thread: row tid / 4 of the tile, 16 columns.
 __global__ __launch_bounds__(256) void k_apply_s(const Phase P) {
+  __shared__ uint16_t tt[64][64 + 2];
   const Loc L = locate(P, blockIdx.x);
   const Entry& E = P.e[L.ent];
-  const int64_t kp = E.kp;
+  const int kp = int(E.kp);
   char* w = ws_of(P, E, L.mat);
   const WsLayout WL = ws_layout(E.kp, E.Np, 2);
   const float* s = reinterpret_cast<const float*>(w + WL.s);
-  const int64_t idx = int64_t(L.tile) * kElemBlock + int64_t(threadIdx.x) * 8;
-  if (idx >= kp * kp) return;
   const float* A0 = reinterpret_cast<const float*>(w + WL.a32);
   uint16_t* A = reinterpret_cast<uint16_t*>(w + WL.a);
-  const int64_t i = idx / kp, j = idx - i * kp;   // kp % 8 == 0: the 8 stay in row i
+  int I, J;
+  tri_tile(L.tile, kp / 64, I, J);
+  const int r = int(threadIdx.x) >> 2, c0 = (int(threadIdx.x) & 3) * 16;
+  const int i = I * 64 + r, j0 = J * 64 + c0;
   const float si = s[i];
-  uint16_t o[8];
+  const float* src = A0 + int64_t(i) * kp + j0;
+  uint16_t o[16];
 #pragma unroll
-  for (int e = 0; e < 8; ++e) o[e] = f2bf(A0[idx + e] * (si * s[j + e]));
-  *reinterpret_cast<uint4*>(A + i * WL.ldg + j) = *reinterpret_cast<const uint4*>(o);
+  for (int q = 0; q < 4; ++q) {
+    const float4 v = *reinterpret_cast<const float4*>(src + 4 * q);
+    o[4 * q + 0] = f2bf(v.x * (si * s[j0 + 4 * q + 0]));
+    o[4 * q + 1] = f2bf(v.y * (si * s[j0 + 4 * q + 1]));
+    o[4 * q + 2] = f2bf(v.z * (si * s[j0 + 4 * q + 2]));
+    o[4 * q + 3] = f2bf(v.w * (si * s[j0 + 4 * q + 3]));
+  }
+  uint16_t* dst = A + int64_t(i) * WL.ldg + j0;
+  reinterpret_cast<uint4*>(dst)[0] = reinterpret_cast<const uint4*>(o)[0];
+  reinterpret_cast<uint4*>(dst)[1] = reinterpret_cast<const uint4*>(o)[1];
+  if (I == J) return;   // uniform per block
+#pragma unroll
+  for (int e = 0; e < 16; ++e) tt[r][c0 + e] = o[e];
+  __syncthreads();
+  // mirror row J*64 + r, columns I*64 + c0 .. + 15 = tile column r
+  uint16_t m[16];
+#pragma unroll
+  for (int e = 0; e < 16; ++e) m[e] = tt[c0 + e][r];
+  uint16_t* d2 = A + int64_t(J * 64 + r) * WL.ldg + I * 64 + c0;
+  reinterpret_cast<uint4*>(d2)[0] = reinterpret_cast<const uint4*>(m)[0];
+  reinterpret_cast<uint4*>(d2)[1] = reinterpret_cast<const uint4*>(m)[1];
 }
 
 #define TM_LAUNCH(kern) \

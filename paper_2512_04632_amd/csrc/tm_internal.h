@@ -139,7 +139,7 @@ TM_HD uint32_t blocks_per_matrix(int kind, int cfg, uint32_t k, uint32_t N, uint
     case kKindUpdate: return cdiv(kp, T) * cdiv(Np, T);
     case kKindApplyScale:
     case kKindCopyOut: return uint32_t((uint64_t(k) * N + kElemBlock - 1) / kElemBlock);
-    case kKindScaleA: return uint32_t((uint64_t(kp) * kp + kElemBlock - 1) / kElemBlock);
+    case kKindScaleA: return tri(kp / 64u);   // upper 64 x 64 tiles (kp % 64 == 0)
   }
   return 0;
 }
