@@ -189,14 +189,6 @@ __device__ inline void dma_wait_upto(int stages) {
   dma_wait<0>();
 }
 
-template <int PS>
-__device__ inline void dma_wait_stages(int stages) {
-  if (stages >= 3) dma_wait<3 * PS>();
-  else if (stages == 2) dma_wait<2 * PS>();
-  else if (stages == 1) dma_wait<PS>();
-  else dma_wait<0>();
-}
-
 __device__ inline void barrier_pinned() {
   __builtin_amdgcn_sched_barrier(0);
   asm volatile("s_barrier" ::: "memory");
@@ -265,12 +257,6 @@ __device__ inline void dma_rm(const uint16_t* src, int64_t ld, int k0, uint32_t 
   const int c = (p16 >> 1) ^ swz_y<T>(r);
   const uint32_t voff = uint32_t((int64_t(r) * ld + c * 16 + (p16 & 1) * 8) * 2);
   dma16(base, voff, __builtin_amdgcn_readfirstlane(lds + uint32_t(j) * 1024u));
-}
-
-template <int T, int BK>
-__device__ inline void issue_rm(const uint16_t* src, int64_t ld, int k0, uint32_t lds) {
-#pragma unroll
-  for (int q = 0; q < Ring<T, BK>::DMA_OP; ++q) dma_rm<T, BK>(src, ld, k0, lds, q);
 }
 
 // ---------------------------------------------------------------- compute
