@@ -650,10 +650,13 @@ __global__ __launch_bounds__(256) void k_aol_vector(const Phase P) {
   if (i < k) {
     if (P.flags & kFrob) {
       const float* fp = reinterpret_cast<const float*>(w + WL.fpart);
+#pragma unroll 8
       for (int b = 0; b < kFrobBlocks; ++b) r += fp[b];
     } else {
+      // unrolled so that the loads are in flight together; the sum keeps its order
       const float* part = reinterpret_cast<const float*>(w + WL.part);
       const int nb = int(cdiv(E.kp, uint32_t(P.aux)));
+#pragma unroll 8
       for (int b = 0; b < nb; ++b) r += part[int64_t(b) * kp + i];
     }
   }
