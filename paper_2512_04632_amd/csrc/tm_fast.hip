@@ -1,16 +1,17 @@
 // bf16 matrix-core path of the Turbo-Muon orthogonalizer for gfx950 (MI355X).
 //
-// Every matrix is held in a zero-padded workspace copy whose dims are
+// Every matrix is processed in a zero-padded workspace layout whose dims are
 // multiples of the square tile T (256, 128 or 64), so every tile is full: the
 // main loops carry no bounds checks and zero padding is preserved by the
-// iteration (padded rows and columns of Y, A and B stay zero).
+// iteration (padded rows and columns of Y, A and B stay zero).  A wide matrix
+// that needs no padding is read in place by the first iteration.
 //
 // Phases (one launch each over the tiles of all matrices of a call):
 //   k_load_in     W1 = X (wide) or X^T (tall), zero padded
 //   k_gram_fast   A = Y Y^T, upper tiles, mirrored bf16 store; at iteration 1
-//                 the fp32 accumulators are stored instead (A0 is rescaled
-//                 before rounding) and the epilogue emits the AOL row sums
-//                 sum_j |A0_ij| (eq. (aol))
+//                 the fp32 accumulators of the upper tiles are stored instead
+//                 (A0 is rescaled before rounding) and the epilogue emits the
+//                 AOL row sums sum_j |A0_ij| (eq. (aol))
 //   k_apply_s     A1 = diag(s) A0 diag(s), rounded once to bf16, from the
 //                 upper tiles of A0
 //   k_poly_fast   B~ = b A + c A A + a I, upper tiles, mirrored store; at
