@@ -732,13 +732,21 @@ __device__ inline bool run_mainloop(f32x16_t (&acc)[Tile<T>::FM][Tile<T>::FN], c
 // operand rows) then run together on one XCD and hit its L2, while the eight
 // XCDs work on adjacent chunks of the same matrices, so operand panels that
 // leave one L2 are still in the memory-side cache when the next XCD asks for
-// them.  Workgroups past the last full round of 8 chunks keep their index.
+// them.  The workgroups past the last full round of 8 chunks (all of them in
+// a launch of fewer than 256 tiles) split the remaining n tiles the same way:
+// XCD x takes a contiguous run of n / 8 of them, one more for x < n % 8 (XCD
+// x has exactly that many of those workgroups), so the tiles of one matrix
+// still share an L2.
 __device__ inline int xcd_remap(int p, int total) {
   constexpr int C = 32;
   const int full = total / (8 * C) * (8 * C);
-  if (p >= full) return p;
-  const int x = p & 7, j = p >> 3;
-  return ((j / C) * 8 + x) * C + (j % C);
+  if (p < full) {
+    const int x = p & 7, j = p >> 3;
+    return ((j / C) * 8 + x) * C + (j % C);
+  }
+  const int n = total - full, q = p - full;
+  const int x = q & 7, j = q >> 3;
+  return full + x * (n >> 3) + min(x, n & 7) + j;
 }
 
 struct Loc {
