@@ -27,9 +27,8 @@
 // tile one), plus producer waves for the Gram and polynomial.  Each wave
 // accumulates 32 x 32 v_mfma_f32_32x32x16_bf16 blocks.  Operands reach LDS
 // through global_load_lds_dwordx4 (direct to LDS, no VGPR staging) into a
-// ring of stages: two of 64 K elements for the 256 tile's update, five
-// operand slots of 64 K elements for its Gram and polynomial, three or four
-// stages of 32, 64 or 128 for the smaller tiles.  K-contiguous operands are
+// ring of five operand slots of 64 K elements for the 256 tile, three or
+// four stages of 32, 64 or 128 for the smaller tiles.  K-contiguous operands are
 // stored as rows of 2 BK bytes whose 16-byte chunks are XOR-swizzled by row
 // group; the update's Y operand is staged in its row-major layout (BK rows
 // of T bf16) with 32-byte chunks XOR-swizzled per row and read with
@@ -85,8 +84,7 @@ struct Ring {
   static constexpr int RPB = 256 / RB;
   static constexpr int A_BYTES = T * RB;         // one operand stage
   static constexpr int STAGE = 2 * A_BYTES;
-  // the 256 tile's Gram and polynomial keep five operand slots of A_BYTES
-  // (mainloop_pp_kc5)
+  // the 256 tile keeps five operand slots of A_BYTES (mainloop_pp_kc5)
   static constexpr int LDS = T == 256 ? 5 * A_BYTES : NSTAGE * STAGE;
   static constexpr int DMA_OP = T * BK / 512 / Tile<T>::NW;   // 1 KB DMAs per wave per operand
   static constexpr int PER_STAGE = 2 * DMA_OP;
@@ -498,8 +496,7 @@ __device__ inline bool mainloop_pc(f32x16_t (&acc)[Tile<T>::FM][Tile<T>::FN], ch
   return true;
 }
 
-// Ping-pong schedule of the 8-wave tile (two loops below, one per layout of
-// operand b).  Waves 0-3 (group 0) and 4-7 (group 1) occupy one slot per SIMD
+// Ping-pong schedule of the 8-wave tile (mainloop_pp_kc5 below).  Waves 0-3 (group 0) and 4-7 (group 1) occupy one slot per SIMD
 // each; group 1 runs one phase behind, so that while one wave of a SIMD
 // issues the 16 MFMAs of a 32-wide K step from registers, the other issues
 // its DMA and reads its operands of the next step from LDS.  Every phase ends
@@ -509,7 +506,7 @@ __device__ inline bool mainloop_pc(f32x16_t (&acc)[Tile<T>::FM][Tile<T>::FN], ch
 // Stages are 64 K elements wide (two steps), so a K-contiguous row of a
 // stage is one full 128-byte line, which the global -> LDS path moves at
 // twice the rate of 64-byte half lines.  That path takes about 64 bytes per
-// clock and compute unit, so both loops issue one operand stage (32 KB per
+// clock and compute unit, so the loop issues one operand stage (32 KB per
 // workgroup) per step rather than a whole stage every other step.  The data
 // a step reads must be in LDS before group 0's MEM of that step: at the end
 // of the step before, group 0 waits for its own DMAs at the end of its COMP,
@@ -520,118 +517,20 @@ __device__ inline bool mainloop_pc(f32x16_t (&acc)[Tile<T>::FM][Tile<T>::FN], ch
 // and that stall then overlaps the reads' completion instead of delaying
 // their start.
 
-// Ping-pong schedule of the update (operand b = the K x T row-major block of
-// Y).  A stage of b splits into two halves of BK / 2 rows without shortening
-// its 2T-byte row pieces, so the DMA can be spread evenly over the two steps
-// of a stage instead of issued in the first: the first step of stage j
-// issues operand a of stage j + 1, the second issues the second half of b's
-// stage j + 1 and the first half of b's stage j + 2.  That last half goes
-// into the buffer of stage j, whose first half every wave finished reading
-// in the first step (the first step reads K rows 0 .. BK/2 - 1 of b, the
-// second the others; group 1's reads are complete at the barrier that ends
-// its memory phase, group 0's before its compute phase).  Every step ends
-// with that wait protocol, for exactly the data the next step reads;
-// the DMAs issued after that data stay in flight:
-//   end of step 1 of stage j: b's second half of stage j is needed; b's
-//     first half of j + 1 and a of j + 1 (HB + DO instructions) may be pending;
-//   end of step 2: a of j + 1 and b's first half of j + 1 are needed; b's
-//     second half of j + 1 and first half of j + 2 (HB each) may be pending.
-template <int T, bool SWAP, int BK>
-__device__ inline void mainloop_pp_rm(f32x16_t (&acc)[Tile<T>::FM][Tile<T>::FN], char* smem,
-                                      const uint16_t* a, int64_t lda, const uint16_t* b,
-                                      int64_t ldb, int K) {
-  static_assert(Tile<T>::NW == 8, "ping-pong needs two waves per SIMD");
-  using R = Ring<T, BK>;
-  constexpr int S = R::NSTAGE, DO = R::DMA_OP, HB = DO / 2;
-  static_assert(S == 2 && BK == 64, "two stages of two 32-wide steps");
-  static_assert(HB == 2 && Tile<T>::NW * HB * (1024 / (2 * T)) == BK / 2,
-                "dma_rm instructions 0 .. HB-1 of every wave cover the first BK / 2 rows");
-  const int wave = threadIdx.x >> 6;
-  const int wm = wave / 4, wn = wave % 4;
-  const bool g1 = __builtin_amdgcn_readfirstlane(wave) >= 4;
-#pragma unroll
-  for (int fm = 0; fm < Tile<T>::FM; ++fm)
-#pragma unroll
-    for (int fn = 0; fn < Tile<T>::FN; ++fn)
-#pragma unroll
-      for (int v = 0; v < 16; ++v) acc[fm][fn][v] = 0.f;
-
-  const uint32_t lds0 = lds_addr(smem);
-  const int nk = K / BK;
-  auto stage_lds = [&](int kt) { return lds0 + uint32_t((kt % S) * R::STAGE); };
-  auto issue_a = [&](int kt) { issue_kc<T, BK>(a, lda, kt * BK, stage_lds(kt)); };
-  auto issue_b = [&](int kt, int half) {
-#pragma unroll
-    for (int q = 0; q < HB; ++q) dma_rm<T, BK>(b, ldb, kt * BK, stage_lds(kt) + R::A_BYTES, half * HB + q);
-  };
-  auto stage_ptr = [&](int kt) { return smem + (kt % S) * R::STAGE; };
-  // wait at the end of step hs of stage j for what step hs + 1 (or stage j + 1) reads
-  auto wait_step = [&](int j, int hs) {
-    if (hs == 0) {
-      if (j + 1 < nk) dma_wait<HB + DO>();
-      else dma_wait<0>();
-    } else {
-      if (j + 2 < nk) dma_wait<2 * HB>();
-      else if (j + 1 < nk) dma_wait<HB>();
-      else dma_wait<0>();
-    }
-  };
-
-  issue_a(0);
-  issue_b(0, 0);
-  issue_b(0, 1);
-  if (nk > 1) {
-    issue_b(1, 0);
-    __builtin_amdgcn_s_waitcnt(0xC07F);
-    ring_sync_dma<HB>();
-  } else {
-    __builtin_amdgcn_s_waitcnt(0xC07F);
-    ring_sync_dma<0>();
-  }
-  if (g1) barrier_pinned();
-
-  Frags<T> f0, f1;
-  for (int j = 0; j < nk; ++j) {
-    const char* st = stage_ptr(j);
-#pragma unroll
-    for (int hs = 0; hs < 2; ++hs) {
-      // MEM
-      load_frags<T, true, BK>(f0, st, st + R::A_BYTES, 2 * hs, wm, wn);
-      load_frags<T, true, BK>(f1, st, st + R::A_BYTES, 2 * hs + 1, wm, wn);
-      if (hs == 0) {
-        if (j + 1 < nk) issue_a(j + 1);
-      } else {
-        if (j + 1 < nk) issue_b(j + 1, 1);
-        if (j + 2 < nk) issue_b(j + 2, 0);
-      }
-      if (g1) {
-        __builtin_amdgcn_s_waitcnt(0xC07F);   // lgkmcnt(0)
-        wait_step(j, hs);
-      }
-      barrier_pinned();
-      // COMP
-      mma<T, SWAP>(acc, f0);
-      mma<T, SWAP>(acc, f1);
-      if (!g1) wait_step(j, hs);
-      barrier_pinned();
-    }
-  }
-  if (!g1) barrier_pinned();
-  __builtin_amdgcn_s_waitcnt(0xC07F);
-  dma_wait<0>();
-}
-
-// Ping-pong schedule of the Gram and the polynomial (both operands
-// K-contiguous rows, of Y or of A).  Their stages cannot be split along K
-// without halving the 128-byte row pieces, so the ring holds five operand
-// slots of one operand stage each, filled in the order a(0), b(0), a(1),
-// b(1), ...: operand stage i goes into slot i % 5.  The slot of a(j + 2) is that of b(j - 1) and the slot of
+// Ping-pong loop of the 8-wave tile: operand a K-contiguous rows (of Y for
+// the Gram, of A for the polynomial, of B~ for the update), operand b
+// K-contiguous rows too (RM = false) or the update's K x T row-major block of
+// Y (RM = true).  A stage of K-contiguous rows cannot be split along K
+// without halving its 128-byte row pieces, so instead of two stages the ring
+// holds five operand slots of one operand stage each (the whole 160 KB),
+// filled in the order a(0), b(0), a(1), b(1), ...: operand stage i goes into
+// slot i % 5.  The slot of a(j + 2) is that of b(j - 1) and the slot of
 // b(j + 1) that of a(j - 1), both free once stage j - 1 has been read, so the
 // first step of stage j issues b(j + 1) and the second a(j + 2): one operand
 // stage per step.  At the end of stage j's second step every wave waits for
 // a(j + 1) and b(j + 1), leaving a(j + 2) in flight; five consecutive operand
 // stages are live at most (a(j), b(j) read, a(j + 1), b(j + 1), a(j + 2)).
-template <int T, bool SWAP, int BK>
+template <int T, bool RM, bool SWAP, int BK>
 __device__ inline void mainloop_pp_kc5(f32x16_t (&acc)[Tile<T>::FM][Tile<T>::FN], char* smem,
                                        const uint16_t* a, int64_t lda, const uint16_t* b,
                                        int64_t ldb, int K) {
@@ -655,7 +554,14 @@ __device__ inline void mainloop_pp_kc5(f32x16_t (&acc)[Tile<T>::FM][Tile<T>::FN]
   auto slot_lds = [&](int i) { return lds0 + uint32_t((i % SLOTS) * R::A_BYTES); };
   auto slot_ptr = [&](int i) { return smem + (i % SLOTS) * R::A_BYTES; };
   auto issue_a = [&](int kt) { issue_kc<T, BK>(a, lda, kt * BK, slot_lds(2 * kt)); };
-  auto issue_b = [&](int kt) { issue_kc<T, BK>(b, ldb, kt * BK, slot_lds(2 * kt + 1)); };
+  auto issue_b = [&](int kt) {
+    if constexpr (RM) {
+#pragma unroll
+      for (int q = 0; q < DO; ++q) dma_rm<T, BK>(b, ldb, kt * BK, slot_lds(2 * kt + 1), q);
+    } else {
+      issue_kc<T, BK>(b, ldb, kt * BK, slot_lds(2 * kt + 1));
+    }
+  };
 
   issue_a(0);
   issue_b(0);
@@ -676,8 +582,8 @@ __device__ inline void mainloop_pp_kc5(f32x16_t (&acc)[Tile<T>::FM][Tile<T>::FN]
 #pragma unroll
     for (int hs = 0; hs < 2; ++hs) {
       // MEM
-      load_frags<T, false, BK>(f0, sa, sb, 2 * hs, wm, wn);
-      load_frags<T, false, BK>(f1, sa, sb, 2 * hs + 1, wm, wn);
+      load_frags<T, RM, BK>(f0, sa, sb, 2 * hs, wm, wn);
+      load_frags<T, RM, BK>(f1, sa, sb, 2 * hs + 1, wm, wn);
       if (hs == 0) {
         if (j + 1 < nk) issue_b(j + 1);
       } else {
@@ -711,11 +617,8 @@ template <int T, bool RM, bool SWAP, int BK>
 __device__ inline bool run_mainloop(f32x16_t (&acc)[Tile<T>::FM][Tile<T>::FN], char* smem,
                                     const uint16_t* a, int64_t lda, const uint16_t* b,
                                     int64_t ldb, int K) {
-  if constexpr (Tile<T>::NW == 8 && RM) {
-    mainloop_pp_rm<T, SWAP, BK>(acc, smem, a, lda, b, ldb, K);
-    return true;
-  } else if constexpr (Tile<T>::NW == 8) {
-    mainloop_pp_kc5<T, SWAP, BK>(acc, smem, a, lda, b, ldb, K);
+  if constexpr (Tile<T>::NW == 8) {
+    mainloop_pp_kc5<T, RM, SWAP, BK>(acc, smem, a, lda, b, ldb, K);
     return true;
   } else if constexpr (RM) {   // the update's smaller tiles: compute waves issue the DMA
     mainloop<T, RM, SWAP, BK>(acc, smem, a, lda, b, ldb, K);
