@@ -72,7 +72,7 @@ def main(argv=None) -> int:
                          "(for counter runs, where the QR library is not wanted)")
     args = ap.parse_args(argv)
     if args.gpus != 1:
-        print(f"bench.py: this build measures one GPU only (asked for --gpus {args.gpus}); "
+        print(f"bench.py: the benchmark runs on one GPU only (asked for --gpus {args.gpus}); "
               "matrices are independent and would be sharded by count across GPUs, "
               "which is not built here.", file=sys.stderr)
         return 2
