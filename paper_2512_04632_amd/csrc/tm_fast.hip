@@ -28,9 +28,9 @@
 // accumulates 32 x 32 v_mfma_f32_32x32x16_bf16 blocks.  Operands reach LDS
 // through global_load_lds_dwordx4 (direct to LDS, no VGPR staging) into a
 // ring of five operand slots of 64 K elements for the 256 tile, three or
-// four stages of 32, 64 or 128 for the smaller tiles.  K-contiguous operands are
-// stored as rows of 2 BK bytes whose 16-byte chunks are XOR-swizzled by row
-// group; the update's Y operand is staged in its row-major layout (BK rows
+// four stages of 32, 64 or 128 for the smaller tiles.  K-contiguous operands
+// are stored as rows of 2 BK bytes whose 16-byte chunks are XOR-swizzled by
+// row group; the update's Y operand is staged in its row-major layout (BK rows
 // of T bf16) with 32-byte chunks XOR-swizzled per row and read with
 // ds_read_b64_tr_b16, which hands each lane 4 consecutive K values of one
 // column.  Both layouts are free of LDS bank conflicts for the main-loop
@@ -496,10 +496,11 @@ __device__ inline bool mainloop_pc(f32x16_t (&acc)[Tile<T>::FM][Tile<T>::FN], ch
   return true;
 }
 
-// Ping-pong schedule of the 8-wave tile (mainloop_pp_kc5 below).  Waves 0-3 (group 0) and 4-7 (group 1) occupy one slot per SIMD
-// each; group 1 runs one phase behind, so that while one wave of a SIMD
-// issues the 16 MFMAs of a 32-wide K step from registers, the other issues
-// its DMA and reads its operands of the next step from LDS.  Every phase ends
+// Ping-pong schedule of the 8-wave tile (mainloop_pp_kc5 below).  Waves 0-3
+// (group 0) and 4-7 (group 1) occupy one slot per SIMD each; group 1 runs
+// one phase behind, so that while one wave of a SIMD issues the 16 MFMAs of
+// a 32-wide K step from registers, the other issues its DMA and reads its
+// operands of the next step from LDS.  Every phase ends
 // with a workgroup barrier:
 //   group 0: [MEM(h) | COMP(h)] for each 32-wide step h, then one idle phase;
 //   group 1: one idle phase, then [MEM(h) | COMP(h)].
