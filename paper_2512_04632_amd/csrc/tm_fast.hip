@@ -1146,11 +1146,13 @@ __global__ __launch_bounds__(Tile<T>::NT) void k_update_fast(const Phase P) {
 }
 
 // W1 = X (wide) or X^T (tall) in the padded layout, zeros outside the matrix.
-// One block per 64 x 64 tile of W1.  Wide: each thread copies 8 consecutive
-// elements of two rows (16-byte loads where the row allows them); tall: the
-// tile goes through LDS to be transposed.
+// One block per 64 x 64 tile of W1; each thread moves 8 consecutive elements
+// of two rows, with 16-byte loads where the row allows them and 16-byte
+// stores.  Tall: X is N x k row-major and W1's row i is X's column i; the
+// tile goes through LDS, whose rows of 66 elements (33 words, an odd count)
+// spread the column reads over the banks.
 __global__ __launch_bounds__(256) void k_load_in(const Phase P) {
-  __shared__ uint16_t tile[kTransposeTile][kTransposeTile + 2];
+  __shared__ __attribute__((aligned(16))) uint16_t tile[kTransposeTile][kTransposeTile + 2];
   const Loc L = locate(P, blockIdx.x);
   const Entry& E = P.e[L.ent];
   const int k = int(E.k), N = int(E.N);
@@ -1161,15 +1163,34 @@ __global__ __launch_bounds__(256) void k_load_in(const Phase P) {
   uint16_t* W = wbuf(P, E, L.mat, kSlotFirst);
   const bool tall = (E.flags & kTall) != 0u;
   if (tall) {
-    const int c = threadIdx.x & 63, r0 = threadIdx.x >> 6;
-    for (int r = r0; r < kTransposeTile; r += 4) {
-      const int l = tl * kTransposeTile + r, i = ti * kTransposeTile + c;
-      tile[r][c] = (l < N && i < k) ? X[int64_t(l) * k + i] : uint16_t(0);
+    const int c8 = threadIdx.x & 7, r0 = threadIdx.x >> 3;
+    const int i0 = ti * kTransposeTile + c8 * 8;
+    const bool vec = (k % 8) == 0 && (reinterpret_cast<uintptr_t>(X) & 15u) == 0u;
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const int r = r0 + 32 * h, l = tl * kTransposeTile + r;   // tile row r = X row l
+      uint4 v = make_uint4(0u, 0u, 0u, 0u);
+      if (l < N && vec && i0 + 8 <= k) {
+        v = *reinterpret_cast<const uint4*>(X + int64_t(l) * k + i0);
+      } else if (l < N) {
+        uint16_t* e = reinterpret_cast<uint16_t*>(&v);
+        for (int u = 0; u < 8; ++u) e[u] = i0 + u < k ? X[int64_t(l) * k + i0 + u] : uint16_t(0);
+      }
+      uint32_t* d = reinterpret_cast<uint32_t*>(&tile[r][c8 * 8]);   // 4-byte aligned
+      d[0] = v.x;
+      d[1] = v.y;
+      d[2] = v.z;
+      d[3] = v.w;
     }
     __syncthreads();
-    for (int r = r0; r < kTransposeTile; r += 4) {
-      const int i = ti * kTransposeTile + r, l = tl * kTransposeTile + c;
-      W[int64_t(i) * ldy + l] = tile[c][r];
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const int rr = r0 + 32 * h, i = ti * kTransposeTile + rr;   // tile column rr = W1 row i
+      uint4 v;
+      uint16_t* e = reinterpret_cast<uint16_t*>(&v);
+#pragma unroll
+      for (int u = 0; u < 8; ++u) e[u] = tile[c8 * 8 + u][rr];
+      *reinterpret_cast<uint4*>(W + int64_t(i) * ldy + tl * kTransposeTile + c8 * 8) = v;
     }
   } else {
     const bool vec = (N % 8) == 0 && (reinterpret_cast<uintptr_t>(X) & 15u) == 0u;
