@@ -262,52 +262,94 @@ tm_status fire(const Plan& pl, int kind, int cfg, const Phase& P) {
   return TM_OK;
 }
 
-// One launch of `kind` per chunk of at most kMaxEntries items.
+// Entries of one launch: a run of positions [first, first + n) of the launch
+// order.  A run of n > 1 single matrices of one shape whose workspace regions
+// follow each other is one kPtrTab entry; otherwise n = 1.
+struct Run {
+  size_t first, n;
+};
+
+// One launch of `kind` per chunk of at most kMaxEntries entries and kMaxPtrs
+// table pointers.
 tm_status launch(const Plan& pl, int kind, int cfg, int src, int dst, float a, float b, float c,
                  uint32_t flags, int aux, Cover cover = kCoverAll) {
   const std::vector<Item>& items = *pl.items;
-  for (size_t base = 0; base < items.size(); base += tmk::kMaxEntries) {
+  // update launches take their largest products first (the longest tiles
+  // start first); every entry carries its own workspace offset
+  std::vector<size_t> idx(items.size());
+  for (size_t i = 0; i < idx.size(); ++i) idx[i] = i;
+  if (kind == tmk::kKindUpdate)
+    std::stable_sort(idx.begin(), idx.end(), [&](size_t x, size_t y) {
+      const Item& u = items[x];
+      const Item& v = items[y];
+      return double(u.k) * u.k * u.N * u.count > double(v.k) * v.k * v.N * v.count;
+    });
+  auto joins = [&](size_t prev, size_t next) {
+    const Item& u = items[idx[prev]];
+    const Item& v = items[idx[next]];
+    return u.count == 1u && v.count == 1u && u.k == v.k && u.N == v.N && u.kp == v.kp &&
+           u.Np == v.Np && u.tall == v.tall && u.direct == v.direct &&
+           pl.ws_off[idx[next]] == pl.ws_off[idx[prev]] + item_ws(u, pl.esz);
+  };
+  std::vector<std::vector<Run>> chunks(1);
+  int ptrs = 0;
+  for (size_t i = 0; i < idx.size(); ++i) {
+    std::vector<Run>& ch = chunks.back();
+    if (!ch.empty() && joins(i - 1, i)) {
+      Run& r = ch.back();
+      const int need = r.n == 1 ? 2 : 1;   // a run of two starts the table
+      if (ptrs + need <= tmk::kMaxPtrs) {
+        ++r.n;
+        ptrs += need;
+        continue;
+      }
+    }
+    if (ch.size() == size_t(tmk::kMaxEntries) || ptrs == tmk::kMaxPtrs) {
+      chunks.emplace_back();
+      ptrs = 0;
+    }
+    chunks.back().push_back(Run{i, 1});
+  }
+  for (const std::vector<Run>& ch : chunks) {
     Phase P;
     std::memset(&P, 0, sizeof(P));
-    const size_t n = std::min(items.size() - base, size_t(tmk::kMaxEntries));
-    // update launches take their largest products first (the longest tiles
-    // start first); every entry carries its own workspace offset
-    std::vector<size_t> idx(n);
-    for (size_t i = 0; i < n; ++i) idx[i] = base + i;
-    if (kind == tmk::kKindUpdate)
-      std::stable_sort(idx.begin(), idx.end(), [&](size_t x, size_t y) {
-        const Item& u = items[x];
-        const Item& v = items[y];
-        return double(u.k) * u.k * u.N * u.count > double(v.k) * v.k * v.N * v.count;
-      });
     // a call split over several launches picks each launch's tile for that
     // launch's matrices (the last one may be much smaller); a product's
     // arithmetic does not depend on the tile size
     int ccfg = cfg;
-    if (pl.esz == 2 && items.size() > size_t(tmk::kMaxEntries) &&
+    if (pl.esz == 2 && chunks.size() > 1 &&
         (kind == tmk::kKindGram || kind == tmk::kKindPoly || kind == tmk::kKindUpdate)) {
       std::vector<Item> chunk;
-      for (size_t i = 0; i < n; ++i) chunk.push_back(items[idx[i]]);
+      for (const Run& r : ch)
+        for (size_t i = r.first; i < r.first + r.n; ++i) chunk.push_back(items[idx[i]]);
       ccfg = kind == tmk::kKindUpdate
                  ? choose_update_cfg(pl.tcfg, chunk)
                  : choose_sym_cfg(kind, pl.tcfg, chunk, kind == tmk::kKindPoly || flags == 0u);
     }
     uint64_t start = 0;
-    for (size_t i = 0; i < n; ++i) {
-      const Item& it = items[idx[i]];
-      Entry& E = P.e[i];
+    uint32_t xp = 0;
+    const size_t n = ch.size();
+    for (size_t e = 0; e < n; ++e) {
+      const Run& r = ch[e];
+      const Item& it = items[idx[r.first]];
+      Entry& E = P.e[e];
       E.x = it.x;
-      E.ws = pl.ws_off[idx[i]];
+      E.ws256 = uint32_t(pl.ws_off[idx[r.first]] >> 8);
       E.k = it.k;
       E.N = it.N;
       E.kp = it.kp;
       E.Np = it.Np;
-      E.count = it.count;
+      E.count = r.n > 1 ? uint32_t(r.n) : it.count;
       E.flags = (it.tall ? tmk::kTall : 0u) | (it.direct ? tmk::kDirect : 0u);
+      if (r.n > 1) {
+        E.flags |= tmk::kPtrTab;
+        E.xbase = xp;
+        for (size_t i = r.first; i < r.first + r.n; ++i) P.xp[xp++] = items[idx[i]].x;
+      }
       E.tile_start = uint32_t(start);
       const bool skip = (cover == kCoverTall && !it.tall) || (cover == kCoverCopied && it.direct);
       E.tiles_per = skip ? 0u : tmk::blocks_per_matrix(kind, ccfg, it.k, it.N, it.kp, it.Np);
-      start += uint64_t(E.tiles_per) * it.count;
+      start += uint64_t(E.tiles_per) * E.count;
     }
     if (start >= (uint64_t(1) << 31))
       return fail(TM_ERR_UNSUPPORTED, "too many tiles in one launch");
@@ -508,6 +550,8 @@ tm_status run_locked(std::vector<Item>& items, int esz, int iters, const float* 
     pl.ws_off.push_back(total);
     total += item_ws(it, esz);
   }
+  if (total >= (uint64_t(1) << 40))   // entries hold offsets in 256-byte units
+    return fail(TM_ERR_UNSUPPORTED, "workspace of more than 1 TB");
   s = get_workspace(dev, st, size_t(total), &pl.ws);
   if (s != TM_OK) return s;
   return esz == 2 ? plan_bf16(pl, iters, coeffs, precond, tcfg) : plan_f32(pl, iters, coeffs, precond);

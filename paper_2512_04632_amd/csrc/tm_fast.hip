@@ -676,11 +676,12 @@ __device__ inline Loc locate(const Phase& P, int lid) {
 }
 
 __device__ inline char* ws_of(const Phase& P, const Entry& E, int mat) {
-  return P.ws + E.ws + uint64_t(mat) * ws_layout(E.kp, E.Np, 2).total;
+  return P.ws + (uint64_t(E.ws256) << 8) + uint64_t(mat) * ws_layout(E.kp, E.Np, 2).total;
 }
 
-__device__ inline uint16_t* user_of(const Entry& E, int mat) {
-  return reinterpret_cast<uint16_t*>(E.x + uint64_t(mat) * E.k * E.N * 2u);
+__device__ inline uint16_t* user_of(const Phase& P, const Entry& E, int mat) {
+  char* x = (E.flags & kPtrTab) ? P.xp[E.xbase + mat] : E.x + uint64_t(mat) * E.k * E.N * 2u;
+  return reinterpret_cast<uint16_t*>(x);
 }
 
 // Y buffer of a slot (kp x Np, ld ldy): the first slot is W1 (or, for a
@@ -688,7 +689,7 @@ __device__ inline uint16_t* user_of(const Entry& E, int mat) {
 // then W2, W1, ... (the final slot is the caller's matrix, handled by the
 // update).
 __device__ inline uint16_t* wbuf(const Phase& P, const Entry& E, int mat, int slot) {
-  if (slot == kSlotFirst && (E.flags & kDirect)) return user_of(E, mat);
+  if (slot == kSlotFirst && (E.flags & kDirect)) return user_of(P, E, mat);
   const WsLayout L = ws_layout(E.kp, E.Np, 2);
   const bool w1 = slot == kSlotFirst || slot == kSlotAlt2;
   return reinterpret_cast<uint16_t*>(ws_of(P, E, mat) + (w1 ? L.w1 : L.w2));
@@ -1140,9 +1141,9 @@ __global__ __launch_bounds__(Tile<T>::NT) void k_update_fast(const Phase P) {
   if (P.dst != kSlotFinal)
     store_rows<T>(smem, wbuf(P, E, L.mat, P.dst), ldy, int64_t(I) * T, int64_t(Lb) * T);
   else if ((E.flags & kTall) == 0u)
-    store_rows_user<T>(smem, user_of(E, L.mat), k, N, I * T, Lb * T);
+    store_rows_user<T>(smem, user_of(P, E, L.mat), k, N, I * T, Lb * T);
   else
-    store_cols_user<T>(smem, user_of(E, L.mat), k, N, I * T, Lb * T);
+    store_cols_user<T>(smem, user_of(P, E, L.mat), k, N, I * T, Lb * T);
 }
 
 // W1 = X (wide) or X^T (tall) in the padded layout, zeros outside the matrix.
@@ -1159,7 +1160,7 @@ __global__ __launch_bounds__(256) void k_load_in(const Phase P) {
   const int64_t ldy = ws_layout(E.kp, E.Np, 2).ldy;
   const int nI = int(E.kp) / kTransposeTile;
   const int ti = L.tile % nI, tl = L.tile / nI;
-  const uint16_t* X = user_of(E, L.mat);
+  const uint16_t* X = user_of(P, E, L.mat);
   uint16_t* W = wbuf(P, E, L.mat, kSlotFirst);
   const bool tall = (E.flags & kTall) != 0u;
   if (tall) {

@@ -17,10 +17,14 @@ TM_HD uint32_t cdiv(uint32_t a, uint32_t b) { return (a + b - 1u) / b; }
 TM_HD uint32_t kpad(uint32_t k) { return (k + 7u) & ~7u; }   // ld of A and B
 
 // Matrices of one launch are described by up to kMaxEntries entries; an entry
-// covers `count` matrices of one shape stored back to back (a batched call is
-// one entry, a grouped call one entry per matrix).  Bigger groups are split
-// into several launches per phase.
-constexpr int kMaxEntries = 64;
+// covers `count` matrices of one shape, stored back to back (a batched call)
+// or, with kPtrTab, wherever the launch's pointer table puts them (matrices of
+// one shape that follow each other in a grouped call; their workspace regions
+// are consecutive).  Groups that need more entries or pointers are split into
+// several launches per phase.  The descriptor stays within about 3 KB of
+// kernel arguments.
+constexpr int kMaxEntries = 48;
+constexpr int kMaxPtrs = 96;
 
 // Y slots named by the phase descriptors.  A slot resolves per matrix:
 //   slot   wide (m <= n)          tall (m > n)
@@ -55,19 +59,21 @@ constexpr uint32_t kTall = 1u;    // the user matrix is N x k (m > n); work on i
 constexpr uint32_t kDirect = 2u;  // bf16: the user matrix already has the padded layout (wide,
                                   // dims multiples of the tile, 16-byte aligned); iteration 1
                                   // reads it in place of the W1 copy
+constexpr uint32_t kPtrTab = 4u;  // matrix j's user pointer is xp[xbase + j] of the launch
 
 constexpr int kFrobBlocks = 32;   // partial sums of squares per matrix
 constexpr int kMinTile = 64;      // smallest Gram tile: bounds the row-sum partial count
 
 struct Entry {
-  char* x;             // user matrix of element 0
-  uint64_t ws;         // byte offset of element 0's workspace region
+  char* x;             // user matrix of element 0 (without kPtrTab)
+  uint32_t ws256;      // byte offset of element 0's workspace region / 256
   uint32_t k, N;       // wide view: k = min(m, n) rows, N = max(m, n) columns
   uint32_t kp, Np;     // padded workspace dims: rows of Y, A, B and ld of A, B (kp); ld of Y (Np)
   uint32_t count;      // matrices in this entry
-  uint32_t flags;      // kTall
+  uint32_t flags;      // kTall, kDirect, kPtrTab
   uint32_t tile_start; // first logical block of this entry in the launch
   uint32_t tiles_per;  // blocks per matrix in the launch
+  uint32_t xbase;      // with kPtrTab: first pointer of this entry in xp
 };
 
 struct Phase {
@@ -80,7 +86,9 @@ struct Phase {
   uint32_t flags;
   int32_t aux;         // AOL-vector / partial kernels: columns per row partial of the Gram
   int32_t tail_base;   // with kTail: first logical tile (of size 2T) covered by the launch
+  char* xp[kMaxPtrs];  // user matrices of the kPtrTab entries
 };
+static_assert(sizeof(Entry) == 48 && sizeof(Phase) <= 3200, "kernel arguments of one launch");
 
 // Optimizer step (fp32 parameters): elementwise launches over the elements of
 // up to kMaxOptEntries matrices, blocks of kOptBlock elements.

@@ -97,20 +97,21 @@ __device__ inline Loc locate(const Phase& P, int lid) {
 template <typename T>
 __device__ inline char* ws_of(const Phase& P, const Entry& E, int mat) {
   const WsLayout L = ws_layout(E.kp, E.Np, sizeof(T));
-  return P.ws + E.ws + uint64_t(mat) * L.total;
+  return P.ws + (uint64_t(E.ws256) << 8) + uint64_t(mat) * L.total;
 }
 
 template <typename T>
-__device__ inline T* user_of(const Entry& E, int mat) {
-  return reinterpret_cast<T*>(E.x + uint64_t(mat) * E.k * E.N * sizeof(T));
+__device__ inline T* user_of(const Phase& P, const Entry& E, int mat) {
+  char* x = (E.flags & kPtrTab) ? P.xp[E.xbase + mat] : E.x + uint64_t(mat) * E.k * E.N * sizeof(T);
+  return reinterpret_cast<T*>(x);
 }
 
 // Wide-view Y buffer of a slot (ld = N), see tm_internal.h.
 template <typename T>
 __device__ inline T* slot_ptr(const Phase& P, const Entry& E, int mat, int slot) {
   const bool tall = (E.flags & kTall) != 0u;
-  if (!tall && (slot == kSlotFirst || slot == kSlotFinal)) return user_of<T>(E, mat);
-  if (tall && slot == kSlotFinal) return user_of<T>(E, mat);
+  if (!tall && (slot == kSlotFirst || slot == kSlotFinal)) return user_of<T>(P, E, mat);
+  if (tall && slot == kSlotFinal) return user_of<T>(P, E, mat);
   const WsLayout L = ws_layout(E.kp, E.Np, sizeof(T));
   char* w = ws_of<T>(P, E, mat);
   const bool w1 = tall ? (slot == kSlotFirst || slot == kSlotAlt2) : (slot == kSlotAlt1);
@@ -576,7 +577,7 @@ __global__ __launch_bounds__(256) void k_transpose_in(const Phase P) {
   const int k = int(E.k), N = int(E.N);
   const int nI = int(cdiv(E.k, kTransposeTile));
   const int ti = L.tile % nI, tl = L.tile / nI;
-  const T* X = user_of<T>(E, L.mat);
+  const T* X = user_of<T>(P, E, L.mat);
   T* W = slot_ptr<T>(P, E, L.mat, kSlotFirst);
   const int c = threadIdx.x & 63, r0 = threadIdx.x >> 6;
   for (int r = r0; r < kTransposeTile; r += 4) {
@@ -611,7 +612,7 @@ __global__ __launch_bounds__(256) void k_frob_partial(const Phase P) {
   const int64_t total = from_part ? nb * E.k : int64_t(E.k) * E.N;
   const int64_t chunk = (total + kFrobBlocks - 1) / kFrobBlocks;
   const int64_t lo = chunk * L.tile, hi = min(total, lo + chunk);
-  const T* X = user_of<T>(E, L.mat);
+  const T* X = user_of<T>(P, E, L.mat);
   const float* part = reinterpret_cast<const float*>(ws_of<T>(P, E, L.mat) +
                                                      ws_layout(E.kp, E.Np, sizeof(T)).part);
   float x = 0.f;
@@ -670,7 +671,7 @@ __global__ __launch_bounds__(256) void k_apply_scale(const Phase P) {
   const Loc L = locate(P, blockIdx.x);
   const Entry& E = P.e[L.ent];
   const int64_t total = int64_t(E.k) * E.N;
-  T* X = user_of<T>(E, L.mat);
+  T* X = user_of<T>(P, E, L.mat);
   const float* s = reinterpret_cast<const float*>(ws_of<T>(P, E, L.mat) +
                                                   ws_layout(E.kp, E.Np, sizeof(T)).s);
   const bool tall = (E.flags & kTall) != 0u;
@@ -689,7 +690,7 @@ __global__ __launch_bounds__(256) void k_copy_out(const Phase P) {
   const Entry& E = P.e[L.ent];
   const int64_t total = int64_t(E.k) * E.N;
   const T* S = slot_ptr<T>(P, E, L.mat, P.src);
-  T* D = user_of<T>(E, L.mat);
+  T* D = user_of<T>(P, E, L.mat);
   const bool tall = (E.flags & kTall) != 0u;
   const int64_t lo = int64_t(L.tile) * kElemBlock;
   for (int64_t idx = lo + threadIdx.x; idx < min(total, lo + kElemBlock); idx += 256) {

@@ -157,7 +157,8 @@ def test_many_small_matrices_one_stage_loops(m, n):
     """300 matrices padded to 64 x 64: the batched call's first Gram and its updates
     run more than 256 tiles of 64, so their ring stages are 64 wide and K = 64 is a
     single stage (the producer-wave loop and the update loop with one stage); the
-    grouped call splits them over launches of 64 matrices, with other stage widths.
+    grouped call splits them over launches of at most 96 matrices (the pointer table
+    of one launch), with other stage widths.
     Both must agree bit for bit with single calls and stay within the oracle's
     tolerance."""
     log(f"case: batch of 300 {m}x{n} bf16 AOL t=4")
@@ -172,6 +173,26 @@ def test_many_small_matrices_one_stage_loops(m, n):
         assert np.array_equal(from_device(tg[i]), G), i
         assert np.array_equal(gpu_orth(Xs[i], "bf16", 4, "aol"), G), i
         assert relF(G, O.orthogonalize(Xs[i], 4)) <= BF16_TOL, i
+
+
+def test_grouped_entry_and_pointer_limits():
+    """A grouped call whose matrices need more launch entries (runs of one shape share
+    an entry through the pointer table, other matrices take one entry each) and more
+    table pointers than one launch holds: 12 blocks of a run of three 32 x 48 matrices
+    and seven single matrices of other shapes (96 entries), then a run of 100 64 x 64
+    matrices.  Every matrix must equal its single call bit for bit."""
+    log("case: grouped call over the entry and pointer-table limits")
+    block = [(32, 48)] * 3 + [(24, 40), (40, 24), (17, 33), (33, 17), (20, 20), (48, 32), (5, 9)]
+    shapes = block * 12 + [(64, 64)] * 100
+    Xs = [make_input(m, n, 0.8, 5000 + i, "bf16") for i, (m, n) in enumerate(shapes)]
+    ts = [to_device(X, "bf16") for X in Xs]
+    tm.orthogonalize_grouped(ts, 4, None, "aol")
+    torch.cuda.synchronize()
+    for i in list(range(0, 120, 7)) + [120, 150, 215, 216, 219]:
+        G = from_device(ts[i])
+        assert np.array_equal(G, gpu_orth(Xs[i], "bf16", 4, "aol")), i
+    for i in (0, 3, 219):
+        assert relF(from_device(ts[i]), O.orthogonalize(Xs[i], 4)) <= BF16_TOL, i
 
 
 # ----------------------------------------------------------------- grouped workloads
