@@ -419,6 +419,11 @@ tm_status plan_bf16(const Plan& pl, int iters, const float* coeffs, int precond,
   const int gcfg = choose_sym_cfg(tmk::kKindGram, tcfg, *pl.items, true);
   const int pcfg = choose_sym_cfg(tmk::kKindPoly, tcfg, *pl.items, true);
   const int part = tmk::kMinTile;   // the matrix-core Gram emits row partials per 64 columns
+  // AOL with at most 16 row partials per row: the rescale pass sums s itself
+  // (same order as the AOL-vector kernel), one launch fewer per call
+  const bool fuse_s = precond == TM_PRECOND_AOL &&
+                      std::all_of(pl.items->begin(), pl.items->end(),
+                                  [&](const Item& it) { return it.kp <= uint32_t(16 * part); });
   tm_status s = TM_OK;
   if (iters > 0 || from_gram)
     s = launch(pl, tmk::kKindLoadIn, 0, 0, 0, 0.f, 0.f, 0.f, 0u, 0, kCoverCopied);
@@ -446,9 +451,9 @@ tm_status plan_bf16(const Plan& pl, int iters, const float* coeffs, int precond,
     const uint32_t scale = (first && scaled) ? tmk::kScale : 0u;
     const uint32_t gflags = (first ? rflags : 0u) | (scale ? tmk::kA32 : 0u);
     s = launch(pl, tmk::kKindGram, gflags != 0u ? gcfg1 : gcfg, src, 0, 0.f, 0.f, 0.f, gflags, 0);
-    if (s == TM_OK && first && from_gram) s = gram_scale(pl, precond, part);
+    if (s == TM_OK && first && from_gram && !fuse_s) s = gram_scale(pl, precond, part);
     if (s == TM_OK && scale)         // A1 = diag(s) A0 diag(s), one rounding
-      s = launch(pl, tmk::kKindScaleA, 0, 0, 0, 0.f, 0.f, 0.f, 0u, 0);
+      s = launch(pl, tmk::kKindScaleA, 0, 0, 0, 0.f, 0.f, 0.f, fuse_s ? tmk::kFuseS : 0u, part);
     // with `scale` the polynomial stores B~ diag(s) and the update reads X0
     if (s == TM_OK) s = launch(pl, tmk::kKindPoly, pcfg, 0, 0, a, b, c, scale, 0);
     if (s == TM_OK) s = launch(pl, tmk::kKindUpdate, tcfg, src, dst, a, b, c, 0u, 0);

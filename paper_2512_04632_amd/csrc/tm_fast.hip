@@ -13,7 +13,9 @@
 //                 (A0 is rescaled before rounding) and the epilogue emits the
 //                 AOL row sums sum_j |A0_ij| (eq. (aol))
 //   k_apply_s     A1 = diag(s) A0 diag(s), rounded once to bf16, from the
-//                 upper tiles of A0
+//                 upper tiles of A0 (for k <= 1024 it also sums the AOL
+//                 vector s from the row partials, in place of a separate
+//                 launch)
 //   k_poly_fast   B~ = b A + c A A + a I, upper tiles, mirrored store; at
 //                 iteration 1 it stores C = B~ diag(s) instead, so that X1 =
 //                 diag(s) X0 is never formed: B~ X1 = C X0
@@ -1217,31 +1219,54 @@ __global__ __launch_bounds__(256) void k_load_in(const Phase P) {
 // tile whatever its tile size; one block per upper 64 x 64 tile (I <= J)
 // reads it once and writes A1's tile (I, J) and, off the diagonal, its
 // transpose (J, I) through LDS (s_i s_j = s_j s_i, so the mirror holds the
-// same values).  Thread: row tid / 4 of the tile, 16 columns.
+// same values).  Thread: row tid / 4 of the tile, 16 columns.  Under kFuseS
+// the block first forms s for its 64 rows and 64 columns from the Gram's row
+// partials, and the diagonal blocks store s for the first polynomial.
 __global__ __launch_bounds__(256) void k_apply_s(const Phase P) {
   __shared__ uint16_t tt[64][64 + 2];
+  __shared__ float sv[128];   // s of the tile's 64 rows, then of its 64 columns
   const Loc L = locate(P, blockIdx.x);
   const Entry& E = P.e[L.ent];
   const int kp = int(E.kp);
   char* w = ws_of(P, E, L.mat);
   const WsLayout WL = ws_layout(E.kp, E.Np, 2);
-  const float* s = reinterpret_cast<const float*>(w + WL.s);
+  float* s = reinterpret_cast<float*>(w + WL.s);
   const float* A0 = reinterpret_cast<const float*>(w + WL.a32);
   uint16_t* A = reinterpret_cast<uint16_t*>(w + WL.a);
   int I, J;
   tri_tile(L.tile, kp / 64, I, J);
+  if (threadIdx.x < 128) {
+    const int q = int(threadIdx.x);
+    const int x = (q < 64 ? I : J) * 64 + (q & 63);
+    float v;
+    if (P.flags & kFuseS) {
+      // s_x = 1 / sqrt(sum of |A0_xj|), the row partials added in column-block
+      // order exactly as the separate AOL-vector kernel adds them
+      const float* part = reinterpret_cast<const float*>(w + WL.part);
+      const int nb = int(cdiv(E.kp, uint32_t(P.aux)));
+      float rs = 0.f;
+      if (x < int(E.k))
+        for (int b = 0; b < nb; ++b) rs += part[int64_t(b) * kp + x];
+      v = rs >= 1.17549435e-38f ? 1.0f / sqrtf(rs) : 0.f;   // padding rows: 0
+      if (I == J && q < 64) s[x] = v;   // for the first polynomial
+    } else {
+      v = s[x];
+    }
+    sv[q] = v;
+  }
+  __syncthreads();
   const int r = int(threadIdx.x) >> 2, c0 = (int(threadIdx.x) & 3) * 16;
   const int i = I * 64 + r, j0 = J * 64 + c0;
-  const float si = s[i];
+  const float si = sv[r];
   const float* src = A0 + int64_t(i) * kp + j0;
   uint16_t o[16];
 #pragma unroll
   for (int q = 0; q < 4; ++q) {
     const float4 v = *reinterpret_cast<const float4*>(src + 4 * q);
-    o[4 * q + 0] = f2bf(v.x * (si * s[j0 + 4 * q + 0]));
-    o[4 * q + 1] = f2bf(v.y * (si * s[j0 + 4 * q + 1]));
-    o[4 * q + 2] = f2bf(v.z * (si * s[j0 + 4 * q + 2]));
-    o[4 * q + 3] = f2bf(v.w * (si * s[j0 + 4 * q + 3]));
+    o[4 * q + 0] = f2bf(v.x * (si * sv[64 + c0 + 4 * q + 0]));
+    o[4 * q + 1] = f2bf(v.y * (si * sv[64 + c0 + 4 * q + 1]));
+    o[4 * q + 2] = f2bf(v.z * (si * sv[64 + c0 + 4 * q + 2]));
+    o[4 * q + 3] = f2bf(v.w * (si * sv[64 + c0 + 4 * q + 3]));
   }
   uint16_t* dst = A + int64_t(i) * WL.ldg + j0;
   reinterpret_cast<uint4*>(dst)[0] = reinterpret_cast<const uint4*>(o)[0];

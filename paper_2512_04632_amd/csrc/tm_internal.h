@@ -53,6 +53,8 @@ constexpr uint32_t kS4 = 32u;     // with kFrob: s = (sum of the partials)^(-1/4
 constexpr uint32_t kFromPart = 64u;  // Frobenius-partial kernel sums the Gram's row partials
 constexpr uint32_t kTail = 128u;  // matrix-core kernels: blocks are 2 x 2 sub-tiles of the
                                   // tiles of twice their size from tail_base on
+constexpr uint32_t kFuseS = 256u; // bf16 rescale of A0: the AOL vector is summed in the same
+                                  // kernel from the Gram's row partials (aux columns each)
 
 // Entry flags.
 constexpr uint32_t kTall = 1u;    // the user matrix is N x k (m > n); work on its transpose

@@ -195,6 +195,22 @@ def test_grouped_entry_and_pointer_limits():
         assert relF(from_device(ts[i]), O.orthogonalize(Xs[i], 4)) <= BF16_TOL, i
 
 
+def test_fused_aol_vector_matches_separate_launch_bitwise():
+    """With k <= 1024 the rescale pass sums the AOL vector itself; a call that also
+    holds a matrix with k > 1024 takes the separate AOL-vector launch for all of its
+    matrices.  Both add the same row partials in the same order: equal bits."""
+    log("case: fused vs separate AOL vector, bitwise")
+    Xs = [make_input(1100, 1200, 0.8, 71, "bf16"), make_input(300, 700, 0.8, 72, "bf16"),
+          make_input(1024, 1030, 0.8, 73, "bf16")]
+    ts = [to_device(X, "bf16") for X in Xs]
+    tm.orthogonalize_grouped(ts, 4, None, "aol")
+    torch.cuda.synchronize()
+    for i, X in enumerate(Xs):
+        G = from_device(ts[i])
+        assert np.array_equal(G, gpu_orth(X, "bf16", 4, "aol")), i
+        assert relF(G, O.orthogonalize(X, 4)) <= BF16_TOL, i
+
+
 # ----------------------------------------------------------------- grouped workloads
 def run_workload(name, iters=4, precond="aol"):
     shapes = synth.workload_shapes(name)
