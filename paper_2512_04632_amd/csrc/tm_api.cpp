@@ -368,7 +368,8 @@ tm_status launch(const Plan& pl, int kind, int cfg, int src, int dst, float a, f
     // bf16 matrix-core phases on 256 x 256 tiles whose last wave would be at
     // most a quarter full: the full waves run as usual, the remaining tiles as
     // 2 x 2 sub-tiles of 128 x 128 in a second launch that fits in one wave
-    // (same per-element arithmetic, four times the blocks for the idle units).
+    // (same per-element arithmetic, four times the blocks for the idle units);
+    // an update tail of at most 16 tiles as 4 x 4 sub-tiles of 64 x 64.
     const bool mc = kind == tmk::kKindGram || kind == tmk::kKindPoly || kind == tmk::kKindUpdate;
     const int tail = (pl.esz == 2 && ccfg == 0 && mc && P.total > kWave && P.total % kWave <= kWave / 4)
                          ? P.total % kWave
@@ -377,10 +378,11 @@ tm_status launch(const Plan& pl, int kind, int cfg, int src, int dst, float a, f
       P.total -= tail;
       s = fire(pl, kind, ccfg, P);
       Phase Q = P;
-      Q.flags |= tmk::kTail;
+      const bool f4 = kind == tmk::kKindUpdate && 16 * tail <= kWave;
+      Q.flags |= tmk::kTail | (f4 ? tmk::kTail4 : 0u);
       Q.tail_base = P.total;
-      Q.total = 4 * tail;
-      if (s == TM_OK) s = fire(pl, kind, 1, Q);
+      Q.total = (f4 ? 16 : 4) * tail;
+      if (s == TM_OK) s = fire(pl, kind, f4 ? 2 : 1, Q);
     } else {
       s = fire(pl, kind, ccfg, P);
     }

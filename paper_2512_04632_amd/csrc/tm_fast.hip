@@ -1095,23 +1095,25 @@ __global__ __launch_bounds__(Tile<T>::NT) void k_update_fast(const Phase P) {
   constexpr int FM = Tile<T>::FM, FN = Tile<T>::FN;
   // Logical tile -> (block row, block column) in groups of 4 block rows, so
   // that concurrently running tiles share rows of B~.  Under kTail the launch
-  // covers the logical tiles (of size 2T) from P.tail_base on as 2 x 2
-  // sub-tiles, one per block.
+  // covers the logical tiles (of size F T) from P.tail_base on as F x F
+  // sub-tiles, one per block (F = 2, or 4 with kTail4).
   const bool tail = (P.flags & kTail) != 0u;
-  const Loc L = tail ? locate(P, P.tail_base + int(blockIdx.x >> 2))
+  const int F = !tail ? 1 : ((P.flags & kTail4) ? 4 : 2);
+  const int FF = F * F;
+  const Loc L = tail ? locate(P, P.tail_base + int(blockIdx.x) / FF)
                      : locate(P, xcd_remap(blockIdx.x, P.total));
   const Entry& E = P.e[L.ent];
   const int kp = int(E.kp), Np = int(E.Np), k = int(E.k), N = int(E.N);
-  const int TL = tail ? 2 * T : T;
+  const int TL = F * T;
   const int nI = kp / TL, nL = Np / TL;
   constexpr int GM = 4;
   const int grp = L.tile / (GM * nL);
   const int first = grp * GM;
   const int gsz = min(nI - first, GM);
   const int rem = L.tile - grp * GM * nL;
-  const int sub = int(blockIdx.x) & 3;
-  const int I = tail ? 2 * (first + rem % gsz) + (sub >> 1) : first + rem % gsz;
-  const int Lb = tail ? 2 * (rem / gsz) + (sub & 1) : rem / gsz;
+  const int sub = tail ? int(blockIdx.x) % FF : 0;
+  const int I = F * (first + rem % gsz) + sub / F;
+  const int Lb = F * (rem / gsz) + sub % F;
 
   char* w = ws_of(P, E, L.mat);
   const WsLayout WL = ws_layout(E.kp, E.Np, 2);

@@ -53,6 +53,7 @@ constexpr uint32_t kS4 = 32u;     // with kFrob: s = (sum of the partials)^(-1/4
 constexpr uint32_t kFromPart = 64u;  // Frobenius-partial kernel sums the Gram's row partials
 constexpr uint32_t kTail = 128u;  // matrix-core kernels: blocks are 2 x 2 sub-tiles of the
                                   // tiles of twice their size from tail_base on
+constexpr uint32_t kTail4 = 512u; // with kTail (update only): 4 x 4 sub-tiles of a quarter size
 constexpr uint32_t kFuseS = 256u; // bf16 rescale of A0: the AOL vector is summed in the same
                                   // kernel from the Gram's row partials (aux columns each)
 
