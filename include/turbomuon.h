@@ -149,6 +149,31 @@ tm_status tm_muon_step_grouped(float* const* W, const float* const* G, float* co
                                float momentum, int nesterov, float weight_decay, int shape_scale,
                                int iters, const float* coeffs, int precond, void* stream);
 
+/*
+ * tm_orthogonalize_noalloc - tm_orthogonalize for callers that cannot allocate
+ * device memory: code under HIP graph capture, tight serving loops, harnesses
+ * that forbid hipMalloc.  Same arguments, kernels and launch plan as
+ * tm_orthogonalize (results are bitwise equal to it), but the workspace is a
+ * static device array of TM_NOALLOC_SCRATCH_BYTES per GPU, placed with the
+ * library's code object and held until the process ends, instead of the
+ * per-stream cache.  The call allocates nothing, frees nothing and
+ * synchronises nothing; the timing hooks do not apply to it.
+ *
+ *   Limit   the call's workspace (tm_workspace_bytes over `batch` copies of
+ *           the shape m x n, dtype_bytes 2) must fit in
+ *           TM_NOALLOC_SCRATCH_BYTES: e.g. one 2048 x 2048 matrix (48 MiB),
+ *           one 1024 x 4096 (24 MiB) or a batch of 4 of 768 x 3072 (54 MiB);
+ *           a larger call returns TM_ERR_UNSUPPORTED before anything is
+ *           enqueued.
+ *   Sharing every call on one GPU uses that GPU's one array: calls that
+ *           overlap in time on a GPU (other streams or host threads) race and
+ *           must be serialised by the caller.  The array keeps the last call's
+ *           contents; nothing in it needs to start at zero.
+ */
+#define TM_NOALLOC_SCRATCH_BYTES 67108864   /* 64 MiB */
+tm_status tm_orthogonalize_noalloc(void* X, int64_t m, int64_t n, int64_t batch, int iters,
+                                   const float* coeffs, int precond, void* stream);
+
 /* Bytes of workspace a call with these shapes needs (0 on invalid shapes).
  * dtype_bytes is 2 (bf16) or 4 (fp32). */
 uint64_t tm_workspace_bytes(const int64_t* m, const int64_t* n, int64_t count,

@@ -50,6 +50,9 @@ _SIGNATURES = {
                                             ctypes.c_int64, ctypes.c_float, ctypes.c_float,
                                             ctypes.c_int, ctypes.c_float, ctypes.c_int,
                                             ctypes.c_int, _c_fp, ctypes.c_int, ctypes.c_void_p]),
+    "tm_orthogonalize_noalloc": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int64, ctypes.c_int64,
+                                                ctypes.c_int64, ctypes.c_int, _c_fp, ctypes.c_int,
+                                                ctypes.c_void_p]),
     "tm_workspace_bytes": (ctypes.c_uint64, [_c_i64p, _c_i64p, ctypes.c_int64, ctypes.c_int]),
     "tm_release_workspaces": (ctypes.c_int, []),
     "tm_timing_enable": (ctypes.c_int, [ctypes.c_int]),
@@ -154,6 +157,30 @@ def orthogonalize(x, iters: int = 4, coeffs: Optional[Sequence] = None, precond=
         st = getattr(lib(), fn)(ctypes.c_void_p(x.data_ptr()), m, n, batch, int(iters),
                                 carr, _precond(precond), ctypes.c_void_p(_stream_handle(x, stream)))
     _check(fn, st)
+    return x
+
+
+TM_NOALLOC_SCRATCH_BYTES = 64 << 20
+
+
+def orthogonalize_noalloc(x, iters: int = 4, coeffs: Optional[Sequence] = None, precond="aol",
+                          stream=None):
+    """tm_orthogonalize_noalloc: as orthogonalize for a bf16 (m, n) or (batch, m, n)
+    tensor, with the workspace in the library's static per-GPU scratch array instead
+    of an allocated one (raises TurboMuonError if the call needs more).  Returns x."""
+    import torch
+    if not x.is_cuda or not x.is_contiguous() or x.dim() not in (2, 3):
+        raise ValueError("x must be a contiguous (m, n) or (batch, m, n) device tensor")
+    if x.dtype != torch.bfloat16:
+        raise ValueError("x must be bfloat16")
+    m, n = int(x.shape[-2]), int(x.shape[-1])
+    batch = int(x.shape[0]) if x.dim() == 3 else 1
+    carr = _coeff_array(iters, coeffs)
+    with torch.cuda.device(x.device):
+        st = lib().tm_orthogonalize_noalloc(ctypes.c_void_p(x.data_ptr()), m, n, batch,
+                                            int(iters), carr, _precond(precond),
+                                            ctypes.c_void_p(_stream_handle(x, stream)))
+    _check("tm_orthogonalize_noalloc", st)
     return x
 
 

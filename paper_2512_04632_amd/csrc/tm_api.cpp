@@ -201,6 +201,7 @@ struct Plan {
   int esz;
   hipStream_t st;
   int tcfg = 0;                   // bf16: the call's layout tile
+  bool timed = true;              // the timing hooks may bracket this call's launches
 };
 
 // bf16 update of one launch of a call split over several launches: the
@@ -242,7 +243,7 @@ int k_step(int kind, int cfg, const Phase& P) {
 // timing hooks are on).
 tm_status fire(const Plan& pl, int kind, int cfg, const Phase& P) {
   TimedLaunch tl{kind, nullptr, nullptr};
-  if (g_timing && P.total > 0) {
+  if (g_timing && pl.timed && P.total > 0) {
     if (hipEventCreate(&tl.start) != hipSuccess || hipEventCreate(&tl.stop) != hipSuccess)
       return fail(TM_ERR_HIP, "hipEventCreate failed");
     (void)hipEventRecord(tl.start, pl.st);
@@ -521,9 +522,13 @@ tm_status plan_f32(const Plan& pl, int iters, const float* coeffs, int precond) 
   return s;
 }
 
-// Plan and enqueue one call (g_mu held, device checked).
+// Plan and enqueue one call (g_mu held, device checked).  With ext_ws the
+// call runs in that caller-provided device buffer of ext_bytes bytes (the
+// allocation-free entry point) instead of the per-stream workspace cache, and
+// its launches are never bracketed by the timing hooks' events.
 tm_status run_locked(std::vector<Item>& items, int esz, int iters, const float* coeffs,
-                     int precond, hipStream_t st, int dev) {
+                     int precond, hipStream_t st, int dev, char* ext_ws = nullptr,
+                     uint64_t ext_bytes = 0) {
   tm_status s = TM_OK;
   // A call of more than kMaxEntries items runs every phase as several
   // launches; largest products first, so the last, partly filled launch
@@ -559,8 +564,17 @@ tm_status run_locked(std::vector<Item>& items, int esz, int iters, const float* 
   }
   if (total >= (uint64_t(1) << 40))   // entries hold offsets in 256-byte units
     return fail(TM_ERR_UNSUPPORTED, "workspace of more than 1 TB");
-  s = get_workspace(dev, st, size_t(total), &pl.ws);
-  if (s != TM_OK) return s;
+  if (ext_ws != nullptr) {
+    if (total > ext_bytes)
+      return fail(TM_ERR_UNSUPPORTED, "the call needs " + std::to_string(total) +
+                                          " bytes of scratch; the static scratch holds " +
+                                          std::to_string(ext_bytes));
+    pl.ws = ext_ws;
+    pl.timed = false;
+  } else {
+    s = get_workspace(dev, st, size_t(total), &pl.ws);
+    if (s != TM_OK) return s;
+  }
   return esz == 2 ? plan_bf16(pl, iters, coeffs, precond, tcfg) : plan_f32(pl, iters, coeffs, precond);
 }
 
@@ -636,8 +650,8 @@ Item make_item(void* X, int64_t m, int64_t n, int64_t count) {
   return it;
 }
 
-tm_status batched(void* X, int64_t m, int64_t n, int64_t batch, int iters, const float* coeffs,
-                  int precond, void* stream, int esz) {
+tm_status check_batched(void* X, int64_t m, int64_t n, int64_t batch, int iters,
+                        const float* coeffs, int precond, int esz) {
   g_last_error.clear();
   tm_status s = check_common(iters, coeffs, precond);
   if (s != TM_OK) return s;
@@ -649,6 +663,13 @@ tm_status batched(void* X, int64_t m, int64_t n, int64_t batch, int iters, const
   if (reinterpret_cast<uintptr_t>(X) % uintptr_t(esz) != 0)
     return fail(TM_ERR_UNSUPPORTED, "X is not aligned to its element size");
   if (batch > INT32_MAX) return fail(TM_ERR_INVALID_ARG, "batch too large");
+  return TM_OK;
+}
+
+tm_status batched(void* X, int64_t m, int64_t n, int64_t batch, int iters, const float* coeffs,
+                  int precond, void* stream, int esz) {
+  tm_status s = check_batched(X, m, n, batch, iters, coeffs, precond, esz);
+  if (s != TM_OK || batch == 0) return s;
   std::vector<Item> items{make_item(X, m, n, batch)};
   return run(items, esz, iters, coeffs, precond, static_cast<hipStream_t>(stream));
 }
@@ -676,6 +697,34 @@ tm_status grouped(void* const* X, const int64_t* m, const int64_t* n, int64_t co
 }
 
 }  // namespace
+
+namespace tmk {
+
+// Argument checks of tm_orthogonalize (nothing is enqueued).
+tm_status check_batched_bf16(void* X, int64_t m, int64_t n, int64_t batch, int iters,
+                             const float* coeffs, int precond) {
+  return check_batched(X, m, n, batch, iters, coeffs, precond, 2);
+}
+
+// tm_orthogonalize in a caller-provided device buffer `ws` of `ws_bytes`
+// (arguments already checked, batch > 0): the same plan and kernels as the
+// cached-workspace call, so the results are bitwise equal to it.
+tm_status run_batched_bf16_in(void* X, int64_t m, int64_t n, int64_t batch, int iters,
+                              const float* coeffs, int precond, void* stream, char* ws,
+                              uint64_t ws_bytes) {
+  std::vector<Item> items{make_item(X, m, n, batch)};
+  std::lock_guard<std::mutex> lock(g_mu);
+  int dev = 0;
+  tm_status s = check_device(&dev);
+  if (s != TM_OK) return s;
+  return run_locked(items, 2, iters, coeffs, precond, static_cast<hipStream_t>(stream), dev, ws,
+                    ws_bytes);
+}
+
+// Record a failure for tm_last_error().
+tm_status fail_with(tm_status s, const char* msg) { return fail(s, msg); }
+
+}  // namespace tmk
 
 extern "C" {
 
