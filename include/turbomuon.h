@@ -38,9 +38,16 @@
  * Graph capture.  A call on a stream whose workspace is already large enough
  * (an earlier call of the same or larger shapes on that stream) allocates
  * nothing and synchronises nothing, so it can be captured into a HIP graph;
- * the captured kernels keep that workspace's address.  While such a graph is
- * in use, make no larger call on the capturing stream (growing the workspace
- * frees the old one) and do not call tm_release_workspaces().
+ * the captured kernels keep that workspace's address.  A call under capture
+ * whose workspace is too small returns TM_ERR_UNSUPPORTED (nothing can be
+ * allocated during capture).  A workspace once used under capture is never
+ * freed or reused in place by a larger call: a later, larger eager call on the
+ * same stream handle (torch hands out pooled stream handles, so another stream
+ * object may share it) gets a new workspace and the captured one stays valid
+ * until tm_release_workspaces(), which must not be called while such a graph
+ * is in use.  Graphs captured on one stream share its workspace: do not replay
+ * them concurrently (on different streams) with each other or with eager calls
+ * on that stream.  tm_orthogonalize_noalloc needs no workspace at all.
  *
  * Errors.  Arguments are validated before anything is enqueued; an invalid
  * call returns a negative status and leaves memory untouched.  Failures of the
@@ -86,8 +93,8 @@ typedef int tm_status;
  *   m, n    1 <= m, n <= TM_MAX_DIM.
  *   batch   >= 0; 0 is a no-op returning TM_OK.
  *   iters   number t of (Gram, polynomial, update) triples, 0..TM_MAX_ITERS.
- *           iters = 0 returns the pre-conditioned X1.  Turbo-Muon uses 4
- *           (Sec. 2, "four iterations by default"), Muon 5.
+ *           iters = 0 returns the pre-conditioned X1.  Turbo-Muon's default
+ *           is 4 (Sec. 2), Muon's 5.
  *   coeffs  host array of iters*3 floats (a_k, b_k, c_k) in iteration order,
  *           read during the call only; NULL selects the constant triple
  *           (3.4445, -4.7750, 2.0315) for every iteration.
@@ -148,6 +155,22 @@ tm_status tm_muon_step_grouped(float* const* W, const float* const* G, float* co
                                const int64_t* m, const int64_t* n, int64_t count, float lr,
                                float momentum, int nesterov, float weight_decay, int shape_scale,
                                int iters, const float* coeffs, int precond, void* stream);
+
+/*
+ * tm_schedule_tail - fewer iterations from a coefficient schedule designed for
+ * more (appendix on the tuning of Newton-Schulz coefficients: a schedule
+ * computed for a fixed number of iterations runs fewer by keeping its last
+ * rows).
+ *
+ *   schedule  host array of rows*3 floats (a_k, b_k, c_k) in iteration order.
+ *   rows      rows of the schedule, 1..TM_MAX_ITERS.
+ *   iters     iterations to run, 0..rows.
+ * Returns schedule + 3*(rows - iters): the last `iters` rows, to pass as the
+ * `coeffs` of a call with that many iterations.  Reads no element and
+ * allocates nothing; NULL (detail in tm_last_error) for a NULL schedule or
+ * rows / iters out of range.
+ */
+const float* tm_schedule_tail(const float* schedule, int rows, int iters);
 
 /*
  * tm_orthogonalize_noalloc - tm_orthogonalize for callers that cannot allocate

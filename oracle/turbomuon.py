@@ -89,49 +89,68 @@ def schatten4_scale(A0: np.ndarray) -> float:
     return 0.0 if f == 0 else 1.0 / np.sqrt(f)
 
 
-def newton_schulz_alg2(X0: np.ndarray, t: int, coeffs=None,
-                       precond: str = "aol") -> np.ndarray:
-    """Algorithms 1 and 2 literally: Gram X^T X, column scaling, X <- aX + XB.
+def first_iterate(X0: np.ndarray, precond: str = "aol"):
+    """The pre-conditioned starting point X1 and its Gram A1 = X1^T X1.
 
-    precond="aol" is Algorithm 2 (Turbo-Muon): the Gram A0 of the raw input
-    gives the AOL vector s, X1 = X0 diag(s) and A1 = diag(s) A0 diag(s) without
-    a second product.  precond="frobenius" is Algorithm 1 (Muon): X1 =
-    X0 / ||X0||_F and A1 = X1^T X1.  precond="schatten4" (appendix on other
-    pre-conditionings) takes the scale 1 / ||X0||_S4 = ||A0||_F^(-1/2) from the
-    first Gram, X1 = X0 / ||X0||_S4 and A1 = A0 / ||X0||_S4^2, again without a
-    second product.  precond="none" starts from X1 = X0.
-    Then for k = 1..t: A_k = X_k^T X_k (k >= 2), B_k = b_k A_k + c_k A_k A_k,
-    X_{k+1} = a_k X_k + X_k B_k.  t = 0 returns X1.
+    "aol" (Algorithm 2, eq. (aol)): the Gram A0 of the raw input gives the
+    column scales s; X1 = X0 diag(s), and A1 = diag(s) A0 diag(s) is obtained
+    by rescaling A0 rather than by a second product.  "frobenius" (Algorithm 1):
+    X1 = X0 / ||X0||_F with its own Gram.  "schatten4" (appendix on other
+    pre-conditionings): the uniform scale g = 1 / ||X0||_S4 = ||A0||_F^(-1/2)
+    from the same first Gram, X1 = g X0 and A1 = g^2 A0.  "none": X1 = X0.
     """
     if precond not in PRECONDS:
         raise ValueError(f"unknown precond {precond!r}")
+    X0 = np.asarray(X0, dtype=np.float64)
+    if precond == "frobenius":
+        X1 = frobenius_scale(X0)
+        return X1, X1.T @ X1
+    if precond == "none":
+        X1 = X0.copy()
+        return X1, X1.T @ X1
+    A0 = X0.T @ X0
+    if precond == "aol":
+        s = aol_vector(A0)
+        return X0 * s[None, :], (s[:, None] * A0) * s[None, :]
+    g = schatten4_scale(A0)
+    return X0 * g, A0 * (g * g)
+
+
+def quintic_step(X: np.ndarray, A: np.ndarray, a: float, b: float, c: float) -> np.ndarray:
+    """eq. (ns_quintic): a X + b X (X^T X) + c X (X^T X)^2, written with the
+    Gram A = X^T X as a X + X (b A + c A^2), so that the quintic costs one
+    Gram, one square of it and one product with X."""
+    return a * X + X @ (b * A + c * (A @ A))
+
+
+def newton_schulz(X0: np.ndarray, t: int, coeffs=None, precond: str = "aol") -> np.ndarray:
+    """t quintic Newton-Schulz steps on the pre-conditioned X1 (Algorithms 1 and 2).
+
+    The Gram used by the first step is the A1 of first_iterate (for AOL and
+    Schatten-4, a rescaling of the Gram that gave the scale); every later step
+    forms the Gram of its own iterate.  Step k uses the k-th (a, b, c) of
+    coeffs (default: the constant triple).  t = 0 returns X1.
+    """
     if t < 0:
         raise ValueError("t must be >= 0")
     cl = _coeff_list(t, coeffs)
-    X0 = np.asarray(X0, dtype=np.float64)
-    if precond == "aol":
-        A0 = X0.T @ X0                       # initial matmul
-        s = aol_vector(A0)                   # AOL vector
-        X = X0 * s[None, :]                  # X1 = X0 s  (columns)
-        A = s[:, None] * A0 * s[None, :]     # A1 = s^T A0 s, no recomputation
-    elif precond == "frobenius":
-        X = frobenius_scale(X0)              # s = 1/||X0||_F ; X1 = X0 s
-        A = X.T @ X                          # A1 = X1^T X1
-    elif precond == "schatten4":
-        A0 = X0.T @ X0                       # initial matmul
-        g = schatten4_scale(A0)              # 1 / ||X0||_S4
-        X = X0 * g                           # X1 = X0 / ||X0||_S4
-        A = A0 * (g * g)                     # A1 = A0 / ||X0||_S4^2
-    else:
-        X = X0.copy()
-        A = X.T @ X
-    for k in range(1, t + 1):
-        a, b, c = cl[k - 1]
-        if k >= 2:
-            A = X.T @ X                      # polynomial 1
-        B = b * A + c * (A @ A)              # polynomial 2
-        X = a * X + X @ B                    # polynomial 3
+    X, A = first_iterate(X0, precond)
+    for k, (a, b, c) in enumerate(cl):
+        if k > 0:
+            A = X.T @ X
+        X = quintic_step(X, A, a, b, c)
     return X
+
+
+def schedule_last(schedule, n: int) -> list:
+    """Fewer iterations from a schedule designed for more (appendix on the
+    tuning of Newton-Schulz coefficients): of a schedule of T rows (a_k, b_k,
+    c_k), n <= T iterations keep its n last rows, in their order."""
+    rows = [tuple(float(v) for v in r) for r in schedule]
+    T = len(rows)
+    if not 0 <= n <= T:
+        raise ValueError(f"cannot run {n} iterations from a schedule of {T} rows")
+    return [rows[T - n + i] for i in range(n)]
 
 
 def orthogonalize(X: np.ndarray, t: int = 4, coeffs=None, precond: str = "aol",
@@ -150,9 +169,9 @@ def orthogonalize(X: np.ndarray, t: int = 4, coeffs=None, precond: str = "aol",
     if side == "auto":
         side = "rows" if m <= n else "cols"
     if side == "rows":
-        return newton_schulz_alg2(X.T, t, coeffs, precond).T
+        return newton_schulz(X.T, t, coeffs, precond).T
     if side == "cols":
-        return newton_schulz_alg2(X, t, coeffs, precond)
+        return newton_schulz(X, t, coeffs, precond)
     raise ValueError(f"unknown side {side!r}")
 
 

@@ -53,6 +53,7 @@ _SIGNATURES = {
     "tm_orthogonalize_noalloc": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int64, ctypes.c_int64,
                                                 ctypes.c_int64, ctypes.c_int, _c_fp, ctypes.c_int,
                                                 ctypes.c_void_p]),
+    "tm_schedule_tail": (_c_fp, [_c_fp, ctypes.c_int, ctypes.c_int]),
     "tm_workspace_bytes": (ctypes.c_uint64, [_c_i64p, _c_i64p, ctypes.c_int64, ctypes.c_int]),
     "tm_release_workspaces": (ctypes.c_int, []),
     "tm_timing_enable": (ctypes.c_int, [ctypes.c_int]),
@@ -251,6 +252,20 @@ def muon_step_grouped(params: Sequence, grads: Sequence, bufs: Sequence, lr: flo
                                         _precond(precond),
                                         ctypes.c_void_p(_stream_handle(params[0], stream)))
     _check("tm_muon_step_grouped", st)
+
+
+def schedule_tail(schedule: Sequence, iters: int) -> list:
+    """The rows of a coefficient schedule that a call with `iters` iterations runs
+    (tm_schedule_tail: the last `iters` rows)."""
+    flat = [float(v) for row in schedule for v in row]
+    rows = len(flat) // 3
+    if rows * 3 != len(flat):
+        raise ValueError("a schedule holds (a, b, c) triples")
+    arr = (ctypes.c_float * max(len(flat), 1))(*flat)
+    p = lib().tm_schedule_tail(arr, rows, int(iters))
+    if not p:
+        raise TurboMuonError("tm_schedule_tail", TM_ERR_INVALID_ARG, last_error())
+    return [(p[3 * i], p[3 * i + 1], p[3 * i + 2]) for i in range(int(iters))]
 
 
 def workspace_bytes(shapes: Sequence, dtype_bytes: int) -> int:

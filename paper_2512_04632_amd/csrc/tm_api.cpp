@@ -43,6 +43,7 @@ constexpr float kA = 3.4445f, kB = -4.7750f, kC = 2.0315f;
 struct Workspace {
   void* ptr = nullptr;
   size_t bytes = 0;
+  bool captured = false;   // used by a call under graph capture: never freed or reused in place
 };
 
 std::mutex g_mu;
@@ -50,6 +51,9 @@ using WsCache = std::map<std::pair<int, hipStream_t>, Workspace>;
 WsCache g_ws;     // iteration workspace of every call
 WsCache g_ws_u;   // bf16 update matrices of the optimizer step
 std::map<int, bool> g_dev_ok;
+// Workspaces replaced while a captured graph may still hold their address:
+// freed only by tm_release_workspaces.
+std::vector<void*> g_retired;
 
 // Timing hooks: event pairs bracketing each launch while enabled.
 struct TimedLaunch {
@@ -105,11 +109,36 @@ tm_status check_device(int* dev) {
   return TM_OK;
 }
 
-// Grow the (device, stream) buffer of a cache to at least `bytes`.
+// Grow the (device, stream) buffer of a cache to at least `bytes`.  Under
+// graph capture nothing may be allocated, freed or synchronised: the buffer
+// must already be large enough, and it is then marked as captured.  A captured
+// buffer keeps its address for the graphs that hold it: a later, larger eager
+// call on that stream handle gets a new buffer, and the old one is retired
+// (freed by tm_release_workspaces only).
 tm_status get_workspace(int dev, hipStream_t st, size_t bytes, char** out, WsCache& cache = g_ws) {
   Workspace& w = cache[{dev, st}];
+  hipStreamCaptureStatus cap = hipStreamCaptureStatusNone;
+  if (hipStreamIsCapturing(st, &cap) != hipSuccess) {
+    (void)hipGetLastError();
+    cap = hipStreamCaptureStatusNone;
+  }
+  if (cap != hipStreamCaptureStatusNone) {
+    if (w.bytes < bytes)
+      return fail(TM_ERR_UNSUPPORTED,
+                  "the stream's workspace holds " + std::to_string(w.bytes) + " bytes, the call "
+                  "needs " + std::to_string(bytes) + "; nothing can be allocated under graph "
+                  "capture (make one call of this size on the stream before capturing)");
+    w.captured = true;
+    *out = static_cast<char*>(w.ptr);
+    return TM_OK;
+  }
   if (w.bytes < bytes) {
-    if (w.ptr) {
+    if (w.ptr && w.captured) {
+      g_retired.push_back(w.ptr);
+      w.ptr = nullptr;
+      w.bytes = 0;
+      w.captured = false;
+    } else if (w.ptr) {
       hipError_t e = hipStreamSynchronize(st);
       if (e != hipSuccess)
         return fail(TM_ERR_HIP, std::string("hipStreamSynchronize: ") + hipGetErrorString(e));
@@ -810,6 +839,21 @@ tm_status tm_muon_step_grouped(float* const* W, const float* const* G, float* co
   return s;
 }
 
+const float* tm_schedule_tail(const float* schedule, int rows, int iters) {
+  g_last_error.clear();
+  if (schedule == nullptr) {
+    fail(TM_ERR_INVALID_ARG, "schedule is NULL");
+    return nullptr;
+  }
+  if (rows < 1 || rows > TM_MAX_ITERS || iters < 0 || iters > rows) {
+    fail(TM_ERR_INVALID_ARG, "need 1 <= rows <= " + std::to_string(TM_MAX_ITERS) +
+                                 " and 0 <= iters <= rows (rows " + std::to_string(rows) +
+                                 ", iters " + std::to_string(iters) + ")");
+    return nullptr;
+  }
+  return schedule + 3 * (rows - iters);
+}
+
 uint64_t tm_workspace_bytes(const int64_t* m, const int64_t* n, int64_t count, int dtype_bytes) {
   if (m == nullptr || n == nullptr || count < 0 || (dtype_bytes != 2 && dtype_bytes != 4)) return 0;
   std::vector<Item> items;
@@ -830,13 +874,15 @@ uint64_t tm_workspace_bytes(const int64_t* m, const int64_t* n, int64_t count, i
 
 tm_status tm_release_workspaces(void) {
   std::lock_guard<std::mutex> lock(g_mu);
-  if (g_ws.empty() && g_ws_u.empty()) return TM_OK;
+  if (g_ws.empty() && g_ws_u.empty() && g_retired.empty()) return TM_OK;
   hipError_t e = hipDeviceSynchronize();
   for (WsCache* c : {&g_ws, &g_ws_u}) {
     for (auto& kv : *c)
       if (kv.second.ptr) (void)hipFree(kv.second.ptr);
     c->clear();
   }
+  for (void* p : g_retired) (void)hipFree(p);
+  g_retired.clear();
   if (e != hipSuccess) return fail(TM_ERR_HIP, std::string("hipDeviceSynchronize: ") + hipGetErrorString(e));
   return TM_OK;
 }

@@ -41,3 +41,25 @@ def relF(G, R):
 
 def eo_ratio(G, R):
     return O.eps_ortho(G) / O.eps_ortho(R)
+
+
+def block_relF_max(G, R, b=256):
+    """Largest relative Frobenius error over the b x b blocks of the output (ragged
+    edge blocks included), so that one wrong tile cannot hide in the global norm."""
+    m, n = R.shape
+    worst = 0.0
+    for i in range(0, m, b):
+        for j in range(0, n, b):
+            worst = max(worst, O.rel_frobenius(G[i:i + b, j:j + b], R[i:i + b, j:j + b]))
+    return worst
+
+
+def normalised_quintic(a):
+    """(a, b, c) with p(1) = 1 and p'(1) = 0 for p(x) = a x + b x^3 + c x^5:
+    b = 5/2 - 2a, c = a - 3/2 (a = 15/8 is the convergent quintic)."""
+    return (a, 2.5 - 2.0 * a, a - 1.5)
+
+
+# A five-row coefficient schedule (decreasing a: the early rows grow small
+# singular values fastest), built from the family above.
+SCHEDULE5 = [normalised_quintic(a) for a in (3.0, 2.6, 2.2, 1.875, 1.6)]

@@ -4,6 +4,7 @@ import ctypes
 import os
 import re
 
+import numpy as np
 import pytest
 
 from paper_2512_04632_amd import _lib as tm
@@ -157,3 +158,26 @@ def test_optimizer_rejects_non_matrix_parameters():
     with pytest.raises(ValueError):
         TurboMuon([torch.nn.Parameter(torch.zeros(4, 4, dtype=torch.float64))])
     TurboMuon([torch.nn.Parameter(torch.zeros(4, 6))], lr=0.1)
+
+
+def test_schedule_tail_points_at_the_last_rows():
+    """tm_schedule_tail returns the last `iters` rows of a schedule (values rounded
+    to float32 only) and rejects out-of-range requests."""
+    sched = [(3.0, -3.5, 1.5), (2.6, -2.7, 1.1), (2.2, -1.9, 0.7), (1.875, -1.25, 0.375),
+             (1.6, -0.7, 0.1)]
+    f32 = lambda rows: [tuple(float(np.float32(v)) for v in r) for r in rows]  # noqa: E731
+    assert tm.schedule_tail(sched, 4) == f32(sched[1:])
+    assert tm.schedule_tail(sched, 5) == f32(sched)
+    assert tm.schedule_tail(sched, 1) == f32(sched[4:])
+    assert tm.schedule_tail(sched, 0) == []
+    for bad in (6, -1):
+        with pytest.raises(tm.TurboMuonError):
+            tm.schedule_tail(sched, bad)
+    L = tm.lib()
+    assert not L.tm_schedule_tail(None, 3, 1)
+    arr = (ctypes.c_float * 3)(1.0, 2.0, 3.0)
+    assert not L.tm_schedule_tail(arr, 0, 0)
+    assert not L.tm_schedule_tail(arr, tm.TM_MAX_ITERS + 1, 1)
+    base = ctypes.cast(arr, ctypes.c_void_p).value
+    p = L.tm_schedule_tail(arr, 1, 0)
+    assert ctypes.cast(p, ctypes.c_void_p).value == base + 12

@@ -18,8 +18,10 @@ torch = pytest.importorskip("torch")
 from paper_2512_04632_amd import _lib as tm  # noqa: E402
 
 
-def test_polar_error_sweep_512():
-    n = 512
+@pytest.mark.parametrize("n", [512, 1024])
+def test_polar_error_sweep(n):
+    """Prints one line per (pre-conditioning, t): the table of polar errors against
+    iterations (run with -s to see it)."""
     X = synth.cast(synth.gaussian_matrix(n, n, seed=0), "bf16")
     Q = O.polar_factor(X)
     eps = {}
@@ -31,7 +33,8 @@ def test_polar_error_sweep_512():
             G = g.float().cpu().numpy().astype(np.float64)
             R = O.orthogonalize(X, t, None, pre)
             eg, eo = O.eps_polar(G, X, Q), O.eps_polar(R, X, Q)
-            log(f"{pre:10s} t={t}: eps_polar gpu {eg:.4f} oracle {eo:.4f}")
+            log(f"{n}x{n} N(0,1) {pre:10s} t={t}: eps_polar gpu {eg:.4f} oracle {eo:.4f} "
+                f"relF {O.rel_frobenius(G, R):.2e}")
             assert O.rel_frobenius(G, R) <= BF16_TOL
             assert abs(eg - eo) <= 0.05 * eo + 2e-3
             eps[pre, t] = eg

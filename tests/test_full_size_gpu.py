@@ -17,7 +17,7 @@ import pytest
 
 from oracle import turbomuon as O
 from paper_2512_04632_amd import synth
-from gpu_helpers import BF16_TOL, EO_RATIO_TOL, from_device, log
+from gpu_helpers import BF16_TOL, EO_RATIO_TOL, block_relF_max, from_device, log
 
 pytestmark = pytest.mark.gpu
 
@@ -44,9 +44,32 @@ def test_llm8b_4096x14336_batch_of_8():
     G = from_device(B[0])
     R = O.orthogonalize(x0, 4, None, "aol")
     e, r = O.rel_frobenius(G, R), O.eps_ortho(G) / O.eps_ortho(R)
-    log(f"matrix 0: relF={e:.3e} eps_ortho ratio={r:.4f}")
-    assert e <= BF16_TOL and abs(r - 1) <= EO_RATIO_TOL
+    eb = block_relF_max(G, R)
+    log(f"matrix 0: relF={e:.3e} worst 256-block relF={eb:.3e} eps_ortho ratio={r:.4f}")
+    assert e <= BF16_TOL and eb <= BF16_TOL and abs(r - 1) <= EO_RATIO_TOL
     assert torch.isfinite(B.float()).all()
+
+
+def test_llm8b_4096x4096_batch_of_8():
+    """The 4096 x 4096 half of the 8B-class configuration (the size of the paper's
+    Table 1 ablation), drawn as the benchmark draws it: matrix 0 of the batched
+    call against the oracle, globally and per 256 x 256 block; matrix 7 bit for bit
+    against its own call."""
+    log("case: 8 x 4096 x 4096 bf16 power law alpha=0.5 seed=0, batched AOL t=4")
+    X = synth.power_law_batch_device(8, 4096, 4096, 0.5, seed=0, device="cuda")
+    torch.cuda.synchronize()
+    x0 = from_device(X[0])
+    B = X.clone()
+    tm.orthogonalize(B, 4, None, "aol")
+    S7 = _single(X[7])
+    torch.cuda.synchronize()
+    assert torch.equal(B[7], S7)
+    G = from_device(B[0])
+    R = O.orthogonalize(x0, 4, None, "aol")
+    e, r = O.rel_frobenius(G, R), O.eps_ortho(G) / O.eps_ortho(R)
+    eb = block_relF_max(G, R)
+    log(f"matrix 0: relF={e:.3e} worst 256-block relF={eb:.3e} eps_ortho ratio={r:.4f}")
+    assert e <= BF16_TOL and eb <= BF16_TOL and abs(r - 1) <= EO_RATIO_TOL
 
 
 def _block_diagonal_case(m, n, count, seed):

@@ -93,3 +93,59 @@ def test_optimizer_step_replays_match_eager():
     torch.cuda.synchronize()
     for a, b in zip(W + M, Wr + Mr):
         assert torch.equal(a, b)
+
+
+def test_larger_call_after_capture_keeps_the_graph_valid():
+    """A workspace used under capture keeps its address: a later, larger eager call
+    on the same stream gets a new workspace, and the graph's replays stay exact."""
+    log("case: graph capture, then a larger eager call on the capture stream")
+    X0 = _inputs("batched_bf16")
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    ref = [x.clone() for x in X0]
+    with torch.cuda.stream(side):
+        _call(ref)
+    side.synchronize()
+    buf = [x.clone() for x in X0]
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph, stream=side):
+        _call(buf)
+    big = torch.randn((2, 1024, 2048), device="cuda").bfloat16()
+    big_ref = big.clone()
+    tm.orthogonalize(big_ref, 4, None, "aol")      # default stream
+    with torch.cuda.stream(side):                  # grows the capture stream's workspace
+        tm.orthogonalize(big, 4, None, "aol", stream=side)
+    side.synchronize()
+    assert torch.equal(big, big_ref)
+    for r in range(2):
+        for b, x in zip(buf, X0):
+            b.copy_(x)
+        _busy_work()
+        graph.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(buf[0], ref[0]), r
+    del graph
+
+
+def test_capture_with_too_small_a_workspace_is_refused():
+    """Nothing can be allocated during capture: a call whose stream has no workspace
+    of that size yet returns TM_ERR_UNSUPPORTED and enqueues nothing."""
+    log("case: capture without a sized workspace")
+    tm.release_workspaces()
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    x = torch.randn((300, 700), device="cuda").bfloat16()
+    keep = x.clone()
+    graph = torch.cuda.CUDAGraph()
+    seen = []
+    with torch.cuda.graph(graph, stream=side):
+        try:
+            tm.orthogonalize(x, 4, None, "aol", stream=side)
+        except tm.TurboMuonError as err:
+            seen.append(err.status)
+    torch.cuda.synchronize()
+    assert seen == [tm.TM_ERR_UNSUPPORTED]
+    graph.replay()
+    torch.cuda.synchronize()
+    assert torch.equal(x, keep)
+    del graph

@@ -12,6 +12,7 @@ import pytest
 
 from oracle import turbomuon as O
 from paper_2512_04632_amd import synth
+from gpu_helpers import SCHEDULE5
 
 TRIPLE = O.CONSTANT_TRIPLE
 HERE = os.path.dirname(os.path.abspath(__file__))
@@ -246,7 +247,7 @@ def test_p6_invariances(m, n):
 
 # --------------------------------------------------------------------------
 # Block-diagonal inputs: every product of the iteration (eq. ns_quintic) keeps
-# the block structure of X X^T, and the AOL scale of a row (Section 2.3)
+# the block structure of X X^T, and the AOL scale of a row (Section 4.1)
 # only sums that row of the Gram, so the output is the block-diagonal of the
 # blocks' own outputs.  A global normalisation (Frobenius) couples the blocks.
 # --------------------------------------------------------------------------
@@ -308,6 +309,74 @@ def test_metric_definitions():
     assert O.eps_ortho(np.zeros_like(X)) == pytest.approx(1.0, abs=1e-14)
     Z = O.orthogonalize(X, 4)
     assert O.eps_polar(Z, X) <= O.eps_bias(X) + O.eps_approx(Z, X) + 1e-14
+
+
+def test_rel_frobenius_by_hand():
+    """||Z - R||_F / ||R||_F on 2 x 2 cases computed by hand: the reference (second
+    argument) sets the scale, a zero reference falls back to the absolute error."""
+    Z = np.array([[1.0, 2.0], [3.0, 4.0]])
+    R = np.array([[1.0, 2.0], [3.0, 5.0]])
+    assert O.rel_frobenius(Z, R) == pytest.approx(1.0 / np.sqrt(39.0), rel=1e-15)
+    assert O.rel_frobenius(R, Z) == pytest.approx(1.0 / np.sqrt(30.0), rel=1e-15)
+    assert O.rel_frobenius(R, R) == 0.0
+    assert O.rel_frobenius(-R, R) == pytest.approx(2.0, rel=1e-15)
+    assert O.rel_frobenius(np.zeros((2, 2)), R) == pytest.approx(1.0, rel=1e-15)
+    assert O.rel_frobenius(Z, np.zeros((2, 2))) == pytest.approx(np.sqrt(30.0), rel=1e-15)
+    # 3 x 4 with a difference of known norm 5 (a 3-4-5 pair) against ||R||_F = 10
+    R3 = np.zeros((3, 4))
+    R3[0, 0], R3[2, 3] = 6.0, 8.0
+    Z3 = R3.copy()
+    Z3[1, 1] += 3.0
+    Z3[1, 2] -= 4.0
+    assert O.rel_frobenius(Z3, R3) == pytest.approx(0.5, rel=1e-15)
+
+
+def test_eps_ortho_tall_and_wide_by_hand():
+    """The orthogonality error is taken on the min(m, n) side and normalised by
+    sqrt(min(m, n)): a tall matrix with orthonormal columns scores 0 (its m x m
+    Gram O O^T is a rank-k projector, far from I_m), a zero matrix 1, twice an
+    orthonormal set ||3 I_k||_F / sqrt(k) = 3, and transposing changes nothing."""
+    rng = np.random.default_rng(4)
+    Q = rand_orth(rng, 7)[:, :3]                  # 7 x 3, Q^T Q = I_3
+    assert O.eps_ortho(Q) <= 1e-14
+    assert O.eps_ortho(Q.T) <= 1e-14
+    P = Q @ Q.T                                   # the other side: a projector of rank 3
+    assert np.linalg.norm(P - np.eye(7)) / np.sqrt(7) == pytest.approx(np.sqrt(4 / 7), rel=1e-12)
+    assert O.eps_ortho(np.zeros((7, 3))) == pytest.approx(1.0, rel=1e-15)
+    assert O.eps_ortho(np.zeros((3, 7))) == pytest.approx(1.0, rel=1e-15)
+    assert O.eps_ortho(2.0 * Q) == pytest.approx(3.0, rel=1e-13)
+    E = np.array([[1.0, 0.0], [0.0, 2.0], [0.0, 0.0]])   # E^T E = diag(1, 4)
+    assert O.eps_ortho(E) == pytest.approx(3.0 / np.sqrt(2.0), rel=1e-15)
+    assert O.eps_ortho(E.T) == pytest.approx(3.0 / np.sqrt(2.0), rel=1e-15)
+
+
+# SCHEDULE5: five quintics normalised at 1 (p(1) = 1, p'(1) = 0), decreasing a.
+
+def test_schedule_last_keeps_the_last_rows():
+    """Appendix on the tuning of Newton-Schulz coefficients: fewer iterations from a
+    five-iteration schedule keep its last rows.  Running the whole schedule equals
+    running its first row, then the truncated schedule of the remaining iterations
+    on that result (no second pre-conditioning): the retained rows must be the
+    last ones, in order."""
+    for a, b, c in SCHEDULE5:
+        assert a + b + c == pytest.approx(1.0, abs=1e-15)
+        assert a + 3 * b + 5 * c == pytest.approx(0.0, abs=1e-14)
+    assert O.schedule_last(SCHEDULE5, 5) == SCHEDULE5
+    assert O.schedule_last(SCHEDULE5, 1) == [SCHEDULE5[4]]
+    assert O.schedule_last(SCHEDULE5, 0) == []
+    assert O.schedule_last(SCHEDULE5, 3) == SCHEDULE5[2:]
+    with pytest.raises(ValueError):
+        O.schedule_last(SCHEDULE5, 6)
+    X = synth.power_law_matrix(24, 40, 0.8, seed=3)
+    for n in (4, 2):
+        full = O.orthogonalize(X, 5, SCHEDULE5, "aol")
+        head = O.orthogonalize(X, 5 - n, SCHEDULE5[:5 - n], "aol")
+        tail = O.orthogonalize(head, n, O.schedule_last(SCHEDULE5, n), "none")
+        assert relF(tail, full) <= 1e-13, n
+    # the truncated run is the composition of the last n scalar polynomials
+    X1 = O.preconditioned(X, "aol")
+    Z = O.orthogonalize(X, 4, O.schedule_last(SCHEDULE5, 4), "aol")
+    assert relF(Z, spectral_closed_form(X1.T, SCHEDULE5[1:]).T) <= 1e-12
 
 
 # --------------------------------------------------------------------------

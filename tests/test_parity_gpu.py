@@ -4,8 +4,8 @@ import pytest
 
 from oracle import turbomuon as O
 from paper_2512_04632_amd import synth
-from gpu_helpers import (BF16_TOL, F32_TOL, EO_RATIO_TOL, from_device, log, make_input, relF,
-                         eo_ratio, to_device)
+from gpu_helpers import (BF16_TOL, F32_TOL, EO_RATIO_TOL, SCHEDULE5, block_relF_max, from_device,
+                         log, make_input, normalised_quintic, relF, eo_ratio, to_device)
 
 pytestmark = pytest.mark.gpu
 
@@ -31,8 +31,11 @@ def test_single_256_fp32_aol4():
     G = gpu_orth(X, "f32", 4, "aol")
     R = O.orthogonalize(X, 4, None, "aol")
     e = relF(G, R)
-    log(f"relF={e:.3e} eps_polar gpu={O.eps_polar(G, X):.4f} oracle={O.eps_polar(R, X):.4f}")
+    Q = O.polar_factor(X)
+    pg, po = O.eps_polar(G, X, Q), O.eps_polar(R, X, Q)
+    log(f"relF={e:.3e} eps_polar gpu={pg:.4f} oracle={po:.4f}")
     assert e <= F32_TOL
+    assert abs(pg - po) <= 0.05 * po   # distance to the SVD polar factor (Section 3)
 
 
 @pytest.mark.parametrize("precond,iters", [("aol", 4), ("frobenius", 5)])
@@ -65,15 +68,34 @@ def test_shapes(m, n, dtype, precond, iters):
     assert e <= tol(dtype)
 
 
-@pytest.mark.parametrize("m,n", [(1, 65536), (65536, 1), (3, 40000), (40000, 3)])
-@pytest.mark.parametrize("dtype,precond,iters", [("bf16", "aol", 4), ("f32", "aol", 4),
-                                                 ("f32", "frobenius", 5), ("f32", "schatten4", 4)])
+# 3 x 40000 bf16 with Frobenius scaling and 5 iterations misses the bf16
+# tolerance whatever the kernels do: a NumPy model of the bf16 storage points
+# (one rounding per stored X, A, B) gives 3.11e-2 on this input, like the GPU.
+# With k = 3 the constant triple's steep slope near the normalised singular
+# values amplifies the rounding of X over five iterations; over 12 seeds the
+# model exceeds 2e-2 on 6 (median 1.7e-2), and adding a X in the fp32 epilogue
+# instead of folding a into the stored polynomial changes the seeds that fail,
+# not their number (5 of 12).  AOL (4.8e-3) and Schatten-4 (8.5e-3) meet it.
+_BF16_K3_FROB = pytest.mark.xfail(strict=True, reason=(
+    "bf16 storage error amplified past 2e-2 at k = 3, Frobenius, t = 5 (3.1e-2 in the "
+    "rounding model of the same input)"))
+
+
+def _extreme_cases():
+    out = []
+    for m, n in [(1, 65536), (65536, 1), (3, 40000), (40000, 3)]:
+        for dtype, precond, iters in [("bf16", "aol", 4), ("bf16", "frobenius", 5),
+                                      ("bf16", "schatten4", 4), ("f32", "aol", 4),
+                                      ("f32", "frobenius", 5), ("f32", "schatten4", 4)]:
+            marks = (_BF16_K3_FROB,) if (m, n, dtype, precond) == (3, 40000, "bf16",
+                                                                   "frobenius") else ()
+            out.append(pytest.param(m, n, dtype, precond, iters, marks=marks))
+    return out
+
+
+@pytest.mark.parametrize("m,n,dtype,precond,iters", _extreme_cases())
 def test_extreme_aspect_ratios(m, n, dtype, precond, iters):
-    """One side at or near the largest dimension, the other tiny.  (bf16 with a
-    uniform scale and k = 3 is left out: there the constant triple amplifies
-    bf16 rounding past the tolerance whatever the kernels do; a NumPy model of
-    the bf16 rounding points gives the same 3.1e-2 for 3 x 40000, Frobenius,
-    t = 5, as the GPU.)"""
+    """One side at or near the largest dimension, the other tiny."""
     log(f"case: {m}x{n} {dtype} {precond} t={iters}")
     X = make_input(m, n, 0.8, m * 7 + n, dtype)
     G = gpu_orth(X, dtype, iters, precond)
@@ -108,8 +130,7 @@ def test_precond_none_and_iters0_none_is_identity():
 # X1 X1^T X1 (Gram + update), (0,0,1) gives (X1 X1^T)^2 X1 (Gram, poly, update).
 @pytest.mark.parametrize("coeffs", [[(1.0, 0.0, 0.0)], [(0.0, 1.0, 0.0)], [(0.0, 0.0, 1.0)],
                                     [(1.5, -0.5, 0.0)] * 3,
-                                    [(4.0848, -6.8946, 2.9270), (3.9505, -6.3029, 2.6377),
-                                     (3.7418, -5.5913, 2.3037), (2.8769, -3.1427, 1.2046)]])
+                                    [normalised_quintic(a) for a in (3.2, 2.5, 2.0, 1.7)]])
 @pytest.mark.parametrize("dtype", ["bf16", "f32"])
 @pytest.mark.parametrize("m,n", [(130, 250), (250, 130)])
 def test_step_isolating_coefficients(coeffs, dtype, m, n):
@@ -118,6 +139,28 @@ def test_step_isolating_coefficients(coeffs, dtype, m, n):
     G = gpu_orth(X, dtype, len(coeffs), "aol", coeffs)
     R = O.orthogonalize(X, len(coeffs), coeffs, "aol")
     assert relF(G, R) <= tol(dtype)
+
+
+@pytest.mark.parametrize("t", [4, 2])
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+@pytest.mark.parametrize("m,n", [(200, 520), (520, 200)])
+def test_truncated_schedule_runs_the_last_rows(t, dtype, m, n):
+    """Appendix on the tuning of Newton-Schulz coefficients: t iterations from a
+    five-row schedule run its last t rows (tm_schedule_tail), e.g. rows 2..5 for
+    t = 4.  Where the oracle's results for the last and the first t rows are far
+    enough apart for the tolerance to tell them apart, the GPU result must also be
+    far from the first rows' (fp64: 8e-3 apart at t = 4, 0.6 at t = 2)."""
+    log(f"case: last {t} rows of a 5-row schedule, {m}x{n} {dtype}")
+    rows = tm.schedule_tail(SCHEDULE5, t)
+    X = make_input(m, n, 0.8, 21, dtype)
+    G = gpu_orth(X, dtype, t, "aol", rows)
+    R = O.orthogonalize(X, t, O.schedule_last(SCHEDULE5, t), "aol")
+    e = relF(G, R)
+    log(f"relF={e:.3e}")
+    assert e <= tol(dtype)
+    W = O.orthogonalize(X, t, SCHEDULE5[:t], "aol")
+    if relF(W, R) > 20 * tol(dtype):
+        assert relF(G, W) > 10 * tol(dtype)
 
 
 def test_zero_matrix_and_zero_row():
@@ -222,30 +265,35 @@ def run_workload(name, iters=4, precond="aol"):
     return Xs, [from_device(t) for t in ts]
 
 
+def _check_group(Xs, Gs):
+    """Every matrix of a grouped call against the oracle: global and per 256 x 256
+    block relative error, and the polar-error ratio."""
+    worst, worst_b = 0.0, 0.0
+    for i, (X, G) in enumerate(zip(Xs, Gs)):
+        R = O.orthogonalize(X, 4)
+        e, r, eb = relF(G, R), eo_ratio(G, R), block_relF_max(G, R)
+        worst, worst_b = max(worst, e), max(worst_b, eb)
+        assert e <= BF16_TOL and eb <= BF16_TOL and abs(r - 1) <= EO_RATIO_TOL, (i, e, eb, r)
+    log(f"{len(Xs)} matrices: worst relF={worst:.3e}, worst 256-block relF={worst_b:.3e}")
+
+
 def test_grouped_gpt2_small_72_matrices():
     log("case: grouped gpt2_small_12layer (72 matrices)")
     Xs, Gs = run_workload("gpt2_small_12layer")
-    worst = 0.0
-    for i, (X, G) in enumerate(zip(Xs, Gs)):
-        if i % 6 and i < 48:
-            continue                      # every 6th attention matrix, all MLP matrices
-        R = O.orthogonalize(X, 4)
-        e, r = relF(G, R), eo_ratio(G, R)
-        worst = max(worst, e)
-        assert e <= BF16_TOL and abs(r - 1) <= EO_RATIO_TOL, (i, e, r)
-    log(f"worst relF={worst:.3e}")
+    _check_group(Xs, Gs)
 
 
 def test_grouped_gpt2_small_matches_single_calls_bitwise():
-    """The grouped call runs 256-tiles (its last update tiles, those of the last tall
-    matrix, as 128 x 128 sub-tiles); a single 3072 x 768 call runs 64-tiles.  Every
+    """The grouped call runs 256-tiles (after the sort by product size its last 16
+    update tiles belong to the last two 768 x 768 matrices, 46 and 47, and run as
+    4 x 4 sub-tiles of 64 x 64); a single 3072 x 768 call runs 64-tiles.  Every
     output element sees the same products in the same order: equal bits."""
     log("case: grouped gpt2_small_12layer vs single calls, bitwise")
     shapes = synth.workload_shapes("gpt2_small_12layer")
     Xs = [make_input(m, n, a, s, "bf16") for (m, n, a, s) in shapes]
     ts = [to_device(X, "bf16") for X in Xs]
     tm.orthogonalize_grouped(ts, 4, None, "aol")
-    for i in (0, 47, 48, 59, 60, 71):
+    for i in (0, 45, 46, 47, 48, 59, 60, 71):
         assert torch.equal(ts[i], (lambda t: (tm.orthogonalize(t, 4, None, "aol"), t)[1])(
             to_device(Xs[i], "bf16"))), i
     torch.cuda.synchronize()
@@ -254,15 +302,7 @@ def test_grouped_gpt2_small_matches_single_calls_bitwise():
 def test_grouped_resnet_conv_64_matrices():
     log("case: grouped resnet_conv_64 (64 matrices)")
     Xs, Gs = run_workload("resnet_conv_64")
-    worst = 0.0
-    for i, (X, G) in enumerate(zip(Xs, Gs)):
-        if i % 4:
-            continue
-        R = O.orthogonalize(X, 4)
-        e, r = relF(G, R), eo_ratio(G, R)
-        worst = max(worst, e)
-        assert e <= BF16_TOL and abs(r - 1) <= EO_RATIO_TOL, (i, e, r)
-    log(f"worst relF={worst:.3e}")
+    _check_group(Xs, Gs)
 
 
 @pytest.mark.parametrize("m,n", [(768, 3072), (3072, 768)])
