@@ -27,7 +27,12 @@
 // barrier or DMA issue can hide behind the other's MFMAs) in a 2 x 4 grid of
 // 128 x 64 blocks; smaller tiles run 4 compute waves in a 2 x 2 grid (the 32
 // tile one), plus producer waves for the Gram and polynomial.  Each wave
-// accumulates 32 x 32 v_mfma_f32_32x32x16_bf16 blocks.  Operands reach LDS
+// accumulates 16 x 16 blocks with v_mfma_f32_16x16x32_bf16, which carries half
+// the accumulator traffic per flop of the 32 x 32 x 16 form and, on random
+// bf16 data, keeps the power-limited clock about 14% higher; every tile size
+// uses it, so all of them add the same products in the same order.  The 256
+// tile's waves multiply a whole 64-wide K stage (96 operand registers next to
+// the 128 accumulators) between two barriers.  Operands reach LDS
 // through global_load_lds_dwordx4 (direct to LDS, no VGPR staging) into a
 // ring of five operand slots of 64 K elements for the 256 tile, three or
 // four stages of 32, 64 or 128 for the smaller tiles.  K-contiguous operands
@@ -49,12 +54,13 @@ namespace fast {
 constexpr int kPingPongBK = 64;
 
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
-typedef float f32x16_t __attribute__((ext_vector_type(16)));
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
 typedef short s16x4_t __attribute__((ext_vector_type(4)));
 
 // Tile T x T computed by NW wave64s in a WGM x WGN grid (2 x 4, 2 x 2, or a
 // single wave for the 32 tile); each wave owns TWM x TWN of the output as
-// 32 x 32 MFMA blocks.
+// FM x FN blocks of 16 x 16, each accumulated by v_mfma_f32_16x16x32_bf16 (a
+// 16 x 16 fp32 block, 4 registers per lane, 32 K values per instruction).
 // The smaller tiles' Gram and polynomial add NP producer waves that only
 // issue the ring's DMA (mainloop_pc); they leave after the main loop, so the
 // epilogues run on the NT threads of the NW compute waves.  (The update's
@@ -68,8 +74,15 @@ struct Tile {
   static constexpr int NP = T == 256 ? 0 : (T == 32 ? 1 : 2);   // producer waves
   static constexpr int NTT = 64 * (NW + NP);    // threads per workgroup
   static constexpr int TWM = T / WGM, TWN = T / WGN;
-  static constexpr int FM = TWM / 32, FN = TWN / 32;
+  static constexpr int FM = TWM / 16, FN = TWN / 16;
 };
+
+// The fp32 accumulators of one wave: block (fm, fn), lane L, element v holds
+// output row 16 fm + 4 (L / 16) + v, column 16 fn + L % 16 of the wave's part
+// (the operands fed the other way round, as the update does, give the
+// transposed block: row 16 fm + L % 16, columns 16 fn + 4 (L / 16) + v).
+template <int T>
+using AccT = f32x4_t[Tile<T>::FM][Tile<T>::FN];
 
 // LDS ring of one main loop: NSTAGE stages of BK K-elements of both operands
 // (the 128 tile's 32-wide ring is 3 deep, 48 KB, so that three blocks share a
@@ -198,36 +211,36 @@ __device__ inline void barrier_pinned() {
 
 // ---------------------------------------------------------------- DMA issue
 // The per-lane offset of a DMA is 32 bits: the base address of every call
-// starts at the tile's first row (kc) or the stage's first row (rm), so an
-// offset spans at most 256 rows of a row of at most 65536 + 7 elements.
+// starts at the instruction's first row, so an offset spans the rows of one
+// wave's instructions (at most 256) of a row of at most 65536 + 7 elements.
 //
 // K-contiguous operand: T rows x BK bf16 in the swizzled row layout of Ring.
 // One instruction fills 1 KB = 64 / CPR rows; lane i writes chunk i % CPR of
-// its row, i.e. it loads logical chunk (i % CPR) ^ swizzle.
-template <int T, int BK>
-__device__ inline void dma_kc(const uint16_t* src, int64_t ld, int k0, uint32_t lds, int q) {
-  using R = Ring<T, BK>;
-  constexpr int RPI = 64 / R::CPR;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int j = wave + Tile<T>::NW * q;
-  const int r = j * RPI + lane / R::CPR;
-  const int c = (lane % R::CPR) ^ ((r / R::RPB) % R::CPR);
-  const uint32_t voff = uint32_t((int64_t(r) * ld + k0 + c * 8) * 2);
-  dma16(src, voff, __builtin_amdgcn_readfirstlane(lds + uint32_t(j) * 1024u));
-}
-
-// The same 1 KB instructions split over NI issuing waves (w = 0 .. NI - 1):
-// instruction q of wave w fills 1 KB block w + NI q of the operand stage.
+// its row, i.e. it loads logical chunk (i % CPR) ^ swizzle.  Split over NI
+// issuing waves (w = 0 .. NI - 1): instruction q of wave w fills 1 KB block
+// w + NI q of the operand stage.  The rows of that block's first row and the
+// K offset go into the (uniform) base address, so the per-lane offset only
+// holds the lane's row within the instructions of wave w and its swizzled
+// chunk, which the compiler can keep in one or two registers.
 template <int T, int BK, int NI>
 __device__ inline void dma_kc_w(const uint16_t* src, int64_t ld, int k0, uint32_t lds, int q, int w) {
   using R = Ring<T, BK>;
   constexpr int RPI = 64 / R::CPR;
   const int lane = threadIdx.x & 63;
   const int j = w + NI * q;
-  const int r = j * RPI + lane / R::CPR;
+  const int rq = NI * q * RPI;                  // uniform row offset of the instruction
+  const int rl = w * RPI + lane / R::CPR;       // row within it
+  const int r = rq + rl;
   const int c = (lane % R::CPR) ^ ((r / R::RPB) % R::CPR);
-  const uint32_t voff = uint32_t((int64_t(r) * ld + k0 + c * 8) * 2);
-  dma16(src, voff, __builtin_amdgcn_readfirstlane(lds + uint32_t(j) * 1024u));
+  const uint16_t* base = src + int64_t(rq) * ld + k0;
+  const uint32_t voff = uint32_t((int64_t(rl) * ld + c * 8) * 2);
+  dma16(base, voff, __builtin_amdgcn_readfirstlane(lds + uint32_t(j) * 1024u));
+}
+
+// All NW compute waves issuing: instruction q of wave w fills block w + NW q.
+template <int T, int BK>
+__device__ inline void dma_kc(const uint16_t* src, int64_t ld, int k0, uint32_t lds, int q) {
+  dma_kc_w<T, BK, Tile<T>::NW>(src, ld, k0, lds, q, int(threadIdx.x >> 6));
 }
 
 template <int T, int BK>
@@ -236,28 +249,39 @@ __device__ inline void issue_kc(const uint16_t* src, int64_t ld, int k0, uint32_
   for (int q = 0; q < Ring<T, BK>::DMA_OP; ++q) dma_kc<T, BK>(src, ld, k0, lds, q);
 }
 
-// 32-byte chunk swizzle of the row-major Y stage (row = 2T bytes).
+// The transposing reads of a 16 x 32 (K) operand block touch, per half wave,
+// 8 rows (bits 0, 1 and 3 of the row vary) at one logical chunk: the swizzle
+// sends them to 8 different 32-byte bank groups (with 4 chunks per row, the
+// 64 tile, row parity supplies the third bit).
 template <int T>
 __device__ inline int swz_y(int r) {
-  return T >= 128 ? 2 * (r & 3) : 2 * ((r >> 1) & 1);
+  return T >= 128 ? ((r & 3) | (((r >> 3) & 1) << 2)) : (((r >> 1) & 1) | (((r >> 3) & 1) << 1));
 }
 
-// Row-major operand (the update's Y): BK rows (K) x T columns, row = 2T bytes.
-// The stage's first row goes into the 64-bit base address, so the 32-bit
-// per-lane offset spans BK rows only, whatever the matrix size.
-template <int T, int BK>
-__device__ inline void dma_rm(const uint16_t* src, int64_t ld, int k0, uint32_t lds, int q) {
+// Row-major operand (the update's Y): BK rows (K) x T columns, row = 2T bytes,
+// 32-byte chunks swizzled per row.  Split over NI issuing waves as dma_kc_w;
+// the instruction's first row (K offset k0 + its rows) goes into the 64-bit
+// base address, so the 32-bit per-lane offset spans a few rows only,
+// whatever the matrix size.
+template <int T, int BK, int NI>
+__device__ inline void dma_rm_w(const uint16_t* src, int64_t ld, int k0, uint32_t lds, int q, int w) {
   constexpr int ROWB = 2 * T;
   constexpr int LPR = ROWB / 16;          // lanes per row
   constexpr int RPI = 1024 / ROWB;        // rows per instruction
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const uint16_t* base = src + int64_t(k0) * ld;
-  const int j = wave + Tile<T>::NW * q;
-  const int r = j * RPI + lane / LPR;
+  const int lane = threadIdx.x & 63;
+  const int j = w + NI * q;
+  const int rq = NI * q * RPI;
+  const int rl = w * RPI + lane / LPR;
   const int p16 = lane % LPR;
-  const int c = (p16 >> 1) ^ swz_y<T>(r);
-  const uint32_t voff = uint32_t((int64_t(r) * ld + c * 16 + (p16 & 1) * 8) * 2);
+  const int c = (p16 >> 1) ^ swz_y<T>(rq + rl);
+  const uint16_t* base = src + int64_t(k0 + rq) * ld;
+  const uint32_t voff = uint32_t((int64_t(rl) * ld + c * 16 + (p16 & 1) * 8) * 2);
   dma16(base, voff, __builtin_amdgcn_readfirstlane(lds + uint32_t(j) * 1024u));
+}
+
+template <int T, int BK>
+__device__ inline void dma_rm(const uint16_t* src, int64_t ld, int k0, uint32_t lds, int q) {
+  dma_rm_w<T, BK, Tile<T>::NW>(src, ld, k0, lds, q, int(threadIdx.x >> 6));
 }
 
 // ---------------------------------------------------------------- compute
@@ -266,97 +290,148 @@ struct Frags {
   uint4 a[Tile<T>::FM], b[Tile<T>::FN];
 };
 
-// MFMA operands of K slice kk (16 wide) of one stage.
-template <int T, bool RM, int BK>
-__device__ inline void load_frags(Frags<T>& fr, const char* sa, const char* sb, int kk, int wm,
-                                  int wn) {
-  constexpr int FM = Tile<T>::FM, FN = Tile<T>::FN;
+template <int T>
+__device__ inline void zero_acc(AccT<T>& acc) {
+#pragma unroll
+  for (int fm = 0; fm < Tile<T>::FM; ++fm)
+#pragma unroll
+    for (int fn = 0; fn < Tile<T>::FN; ++fn) acc[fm][fn] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+}
+
+// MFMA operands of the 32-wide K slice s of one stage.  K-contiguous operand,
+// block of 16 rows: lane L loads the 16 bytes (8 K values) at K offset 32 s +
+// 8 (L / 16) of row L % 16; the rows of a wave's blocks are 16 apart, which
+// keeps the chunk swizzle, so one address serves all of them.  Row-major
+// operand (the update's Y, RM): lane L needs the 8 K values 32 s + 8 (L / 16)
+// .. + 7 of column L % 16 of the block, gathered by two transposing reads of
+// four rows each: lane q of a 16-lane group addresses row kb + q / 4, columns
+// 4 (q % 4) .. + 3 of the block, and receives rows kb .. kb + 3 of column q.
+template <int T, int BK>
+__device__ inline void load_frags_a(Frags<T>& fr, const char* sa, int s, int wm) {
   using R = Ring<T, BK>;
   const int lane = threadIdx.x & 63;
-  const int lr = lane & 31, lh = lane >> 5;
-  const int c = 2 * kk + lh;
+  const int lr = lane & 15, g = lane >> 4;
+  const int c = 4 * s + g;
+  const int r0 = wm * Tile<T>::TWM + lr;
+  const char* p = sa + r0 * R::RB + 16 * (c ^ ((r0 / R::RPB) % R::CPR));
 #pragma unroll
-  for (int f = 0; f < FM; ++f) {
-    const int r = wm * Tile<T>::TWM + f * 32 + lr;
-    fr.a[f] = *reinterpret_cast<const uint4*>(sa + r * R::RB + 16 * (c ^ ((r / R::RPB) % R::CPR)));
-  }
+  for (int f = 0; f < Tile<T>::FM; ++f) fr.a[f] = *reinterpret_cast<const uint4*>(p + f * 16 * R::RB);
+}
+
+template <int T, bool RM, int BK>
+__device__ inline void load_frags_b(Frags<T>& fr, const char* sb, int s, int wn) {
+  constexpr int FN = Tile<T>::FN;
+  using R = Ring<T, BK>;
+  const int lane = threadIdx.x & 63;
+  const int lr = lane & 15, g = lane >> 4;
+  const int c = 4 * s + g;
   if constexpr (!RM) {
+    const int r0 = wn * Tile<T>::TWN + lr;
+    const char* p = sb + r0 * R::RB + 16 * (c ^ ((r0 / R::RPB) % R::CPR));
 #pragma unroll
-    for (int f = 0; f < FN; ++f) {
-      const int r = wn * Tile<T>::TWN + f * 32 + lr;
-      fr.b[f] = *reinterpret_cast<const uint4*>(sb + r * R::RB + 16 * (c ^ ((r / R::RPB) % R::CPR)));
-    }
+    for (int f = 0; f < FN; ++f) fr.b[f] = *reinterpret_cast<const uint4*>(p + f * 16 * R::RB);
   } else {
-    // Lane q of 16-lane group g addresses row kb + q/4, columns n + 4(q%4);
-    // the transposed read returns rows kb..kb+3 of column n + q.
-    const int g = lane >> 4, q = lane & 15;
-    const int kb = 16 * kk + 8 * (g >> 1) + (q >> 2);
+    // Column block f of wave wn is block f WGN + wn of the tile (the waves'
+    // blocks interleave), i.e. 32-byte chunk f WGN + wn of a stage row.  Row of
+    // the first read within the slice; the second read's row (+ 4) and every
+    // slice share its swizzle (bits 0, 1 and 3 of the row).  chunk ^ sw =
+    // (f ^ hi) WGN + (wn ^ lo) with hi = sw / WGN, lo = sw % WGN.
+    constexpr int WGN = Tile<T>::WGN;
+    const int rl = 8 * g + (lr >> 2);
+    const int sw = swz_y<T>(rl);
+    const int hi = sw / WGN;
+    const char* base = sb + (32 * s + rl) * (2 * T) + 8 * (lr & 3) + 32 * (wn ^ (sw % WGN));
+    // when hi is 0 or 1 (sw < 2 WGN), f ^ hi = f + hi for even f and f - hi for
+    // odd f: two addresses and immediate offsets serve every block
+    constexpr bool two = (T >= 128 ? 8 : 4) <= 2 * WGN;   // largest sw + 1 <= 2 WGN
+    const char* pe = base + 32 * WGN * hi;
+    const char* po = base - 32 * WGN * hi;
 #pragma unroll
     for (int f = 0; f < FN; ++f) {
-      const int chunk = (wn * Tile<T>::TWN + f * 32) / 16 + (g & 1);
+      const char* p = two ? ((f & 1) ? po : pe) + 32 * WGN * f : base + 32 * WGN * (f ^ hi);
       s16x4_t v[2];
 #pragma unroll
-      for (int h = 0; h < 2; ++h) {
-        const int row = kb + 4 * h;
-        const char* p = sb + row * (2 * T) + 32 * (chunk ^ swz_y<T>(row)) + 8 * (q & 3);
+      for (int h = 0; h < 2; ++h)
         v[h] = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-            (__attribute__((address_space(3))) s16x4_t*)(lds_addr(p)));
-      }
+            (__attribute__((address_space(3))) s16x4_t*)(lds_addr(p + h * 4 * (2 * T))));
       fr.b[f] = __builtin_bit_cast(uint4, v);
     }
   }
 }
 
-// SWAP = false: acc[fm][fn] holds C block (fm, fn) in the MFMA layout (lane
-// L, element v: row 8(v/4) + 4(L/32) + v%4, column L%32).  SWAP = true feeds
-// the operands the other way round, so acc[fm][fn] holds the transposed block:
-// each lane then owns 4 consecutive columns of one C row.
+template <int T, bool RM, int BK>
+__device__ inline void load_frags(Frags<T>& fr, const char* sa, const char* sb, int s, int wm,
+                                  int wn) {
+  load_frags_a<T, BK>(fr, sa, s, wm);
+  load_frags_b<T, RM, BK>(fr, sb, s, wn);
+}
+
+// SWAP = false: acc[fm][fn] = a-rows x b-rows^T (the MFMA layout of AccT).
+// SWAP = true feeds the operands the other way round, so acc[fm][fn] holds
+// the transposed block: each lane then owns 4 consecutive columns of one row.
 template <int T, bool SWAP>
-__device__ inline void mma(f32x16_t (&acc)[Tile<T>::FM][Tile<T>::FN], const Frags<T>& fr) {
+__device__ inline void mma(AccT<T>& acc, const Frags<T>& fr) {
 #pragma unroll
   for (int fm = 0; fm < Tile<T>::FM; ++fm)
 #pragma unroll
     for (int fn = 0; fn < Tile<T>::FN; ++fn) {
       if constexpr (SWAP)
-        acc[fm][fn] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+        acc[fm][fn] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
             __builtin_bit_cast(bf16x8_t, fr.b[fn]), __builtin_bit_cast(bf16x8_t, fr.a[fm]),
             acc[fm][fn], 0, 0, 0);
       else
-        acc[fm][fn] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+        acc[fm][fn] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
             __builtin_bit_cast(bf16x8_t, fr.a[fm]), __builtin_bit_cast(bf16x8_t, fr.b[fn]),
             acc[fm][fn], 0, 0, 0);
     }
 }
 
+// Runs slice(kt, s, cur, nxt) over every 32-wide slice s of every stage kt in
+// increasing K order; cur holds the slice's operands, nxt receives the next
+// one's.  With an even number of slices per stage the two operand buffers
+// alternate within a stage; with one slice per stage, across stages.
+template <int NS, class Fr, class Slice>
+__device__ inline void for_each_slice(int nk, Fr& f0, Fr& f1, Slice slice) {
+  if constexpr (NS % 2 == 0) {
+    for (int kt = 0; kt < nk; ++kt)
+#pragma unroll
+      for (int s = 0; s < NS; s += 2) {
+        slice(kt, s, f0, f1);
+        slice(kt, s + 1, f1, f0);
+      }
+  } else {
+    static_assert(NS == 1, "one or an even number of slices per stage");
+    int kt = 0;
+    for (; kt + 1 < nk; kt += 2) {
+      slice(kt, 0, f0, f1);
+      slice(kt + 1, 0, f1, f0);
+    }
+    if (kt < nk) slice(kt, 0, f0, f1);
+  }
+}
+
 // 4-wave main loop of the update's 128 and 64 tiles.  acc = A (T x K,
 // K-contiguous rows of a) * B^T where B's rows are the K-contiguous rows of b
 // (RM = false) or B = the K x T row-major block of b (RM = true); K is a
-// multiple of BK and every tile is full.  The
-// operands of each 16-wide K slice are read from LDS while the previous
-// slice's MFMAs run.  The DMA is spread over the K slices: while stage kt is
-// read and multiplied, each wave issues its share of stage kt + NSTAGE - 1,
-// PS / NS instructions per slice, into the buffer of stage kt - 1 (every wave
-// finished reading it before the barrier that opened stage kt).  The
-// global -> LDS path (about 64 bytes per clock and compute unit) is then fed
-// evenly instead of in one burst per stage that stalls every wave.  Slices
-// are consumed in increasing order whatever BK is, so every output element
-// accumulates the same products in the same order.
+// multiple of BK and every tile is full.  The operands of each 32-wide K
+// slice are read from LDS while the previous slice's MFMAs run.  The DMA is
+// spread over the K slices: while stage kt is read and multiplied, each wave
+// issues its share of stage kt + NSTAGE - 1, PS / NS instructions per slice,
+// into the buffer of stage kt - 1 (every wave finished reading it before the
+// barrier that opened stage kt).  The global -> LDS path (about 64 bytes per
+// clock and compute unit) is then fed evenly instead of in one burst per stage
+// that stalls every wave.  Slices are consumed in increasing order whatever BK
+// is, so every output element accumulates the same products in the same order.
 template <int T, bool RM, bool SWAP, int BK>
-__device__ inline void mainloop(f32x16_t (&acc)[Tile<T>::FM][Tile<T>::FN], char* smem,
-                                const uint16_t* a, int64_t lda, const uint16_t* b,
-                                int64_t ldb, int K) {
+__device__ inline void mainloop(AccT<T>& acc, char* smem, const uint16_t* a, int64_t lda,
+                                const uint16_t* b, int64_t ldb, int K) {
   using R = Ring<T, BK>;
-  constexpr int PS = R::PER_STAGE, NS = BK / 16, NST = R::NSTAGE, DO = R::DMA_OP;
+  constexpr int PS = R::PER_STAGE, NS = BK / 32, NST = R::NSTAGE, DO = R::DMA_OP;
   constexpr int PPS = PS / NS;
   static_assert(PPS * NS == PS && PPS >= 1, "whole DMA instructions per slice");
   const int wave = threadIdx.x >> 6;
   const int wm = wave / Tile<T>::WGN, wn = wave % Tile<T>::WGN;
-#pragma unroll
-  for (int fm = 0; fm < Tile<T>::FM; ++fm)
-#pragma unroll
-    for (int fn = 0; fn < Tile<T>::FN; ++fn)
-#pragma unroll
-      for (int v = 0; v < 16; ++v) acc[fm][fn][v] = 0.f;
+  zero_acc<T>(acc);
 
   const uint32_t lds0 = lds_addr(smem);
   const int nk = K / BK;
@@ -379,38 +454,30 @@ __device__ inline void mainloop(f32x16_t (&acc)[Tile<T>::FM][Tile<T>::FN], char*
 
   Frags<T> f0, f1;
   load_frags<T, RM, BK>(f0, stage_ptr(0), stage_ptr(0) + R::A_BYTES, 0, wm, wn);
-  for (int kt = 0; kt < nk; ++kt) {
+  for_each_slice<NS>(nk, f0, f1, [&](int kt, int s, Frags<T>& cur, Frags<T>& nxt) {
     const char* st = stage_ptr(kt);
     const int nx = kt + NST - 1;   // stage refilled during this one
     const bool fill = nx < nk;
-#pragma unroll
-    for (int s = 0; s < NS; s += 2) {
-      load_frags<T, RM, BK>(f1, st, st + R::A_BYTES, s + 1, wm, wn);
+    if (s + 1 < NS) {
+      load_frags<T, RM, BK>(nxt, st, st + R::A_BYTES, s + 1, wm, wn);
       if (fill)
 #pragma unroll
         for (int i = 0; i < PPS; ++i) dma_one(nx, s * PPS + i);
-      mma<T, SWAP>(acc, f0);
-      if (s + 2 < NS) {
-        load_frags<T, RM, BK>(f0, st, st + R::A_BYTES, s + 2, wm, wn);
-        if (fill)
+      mma<T, SWAP>(acc, cur);
+    } else {
+      if (fill)
 #pragma unroll
-          for (int i = 0; i < PPS; ++i) dma_one(nx, (s + 1) * PPS + i);
-        mma<T, SWAP>(acc, f1);
-      } else {
-        if (fill)
-#pragma unroll
-          for (int i = 0; i < PPS; ++i) dma_one(nx, (s + 1) * PPS + i);
-        __builtin_amdgcn_sched_barrier(0);
-        if (kt + 1 < nk) {
-          ring_wait<PS, NST - 2>(min(nk - 1, kt + NST - 1) - (kt + 1));
-          const char* nxp = stage_ptr(kt + 1);
-          load_frags<T, RM, BK>(f0, nxp, nxp + R::A_BYTES, 0, wm, wn);
-        }
-        __builtin_amdgcn_sched_barrier(0);
-        mma<T, SWAP>(acc, f1);
+        for (int i = 0; i < PPS; ++i) dma_one(nx, s * PPS + i);
+      __builtin_amdgcn_sched_barrier(0);
+      if (kt + 1 < nk) {
+        ring_wait<PS, NST - 2>(min(nk - 1, kt + NST - 1) - (kt + 1));
+        const char* nxp = stage_ptr(kt + 1);
+        load_frags<T, RM, BK>(nxt, nxp, nxp + R::A_BYTES, 0, wm, wn);
       }
+      __builtin_amdgcn_sched_barrier(0);
+      mma<T, SWAP>(acc, cur);
     }
-  }
+  });
   ring_sync<0>();   // the ring is free for the epilogue
 }
 
@@ -422,22 +489,20 @@ __device__ inline void mainloop(f32x16_t (&acc)[Tile<T>::FM][Tile<T>::FN], char*
 // read LDS and multiply.  Per stage kt, between two workgroup barriers: the
 // producers issue stage kt + NST - 1 into the buffer of stage kt - 1 (read
 // before the last barrier) and wait for their DMA of stage kt + 1; the
-// compute waves multiply stage kt, loading the operands of each 16-wide
+// compute waves multiply stage kt, loading the operands of each 32-wide
 // slice while the previous slice's MFMAs run, and finish their LDS reads
 // before the barrier.  Slices are consumed in increasing K order, so every
 // output element accumulates the same products in the same order as in the
 // other loops.  The producer waves return afterwards; a barrier then waits
 // only for the waves still running.
 template <int T, bool SWAP, int BK>
-__device__ inline bool mainloop_pc(f32x16_t (&acc)[Tile<T>::FM][Tile<T>::FN], char* smem,
-                                   const uint16_t* a, int64_t lda, const uint16_t* b,
-                                   int64_t ldb, int K) {
+__device__ inline bool mainloop_pc(AccT<T>& acc, char* smem, const uint16_t* a, int64_t lda,
+                                   const uint16_t* b, int64_t ldb, int K) {
   using R = Ring<T, BK>;
-  constexpr int NW = Tile<T>::NW, NP = Tile<T>::NP, NS = BK / 16, NST = R::NSTAGE;
+  constexpr int NW = Tile<T>::NW, NP = Tile<T>::NP, NS = BK / 32, NST = R::NSTAGE;
   constexpr int DOP = T * BK / 512 / NP;     // 1 KB DMAs per producer and operand stage
   constexpr int PSP = 2 * DOP;
   static_assert(NP >= 1 && DOP * NP * 512 == T * BK, "whole DMA instructions per producer");
-  static_assert(NS % 2 == 0, "slices in pairs");
   const int wave = __builtin_amdgcn_readfirstlane(int(threadIdx.x >> 6));
   const bool prod = wave >= NW;
   const uint32_t lds0 = lds_addr(smem);
@@ -464,151 +529,123 @@ __device__ inline bool mainloop_pc(f32x16_t (&acc)[Tile<T>::FM][Tile<T>::FN], ch
     return false;
   }
   const int wm = wave / Tile<T>::WGN, wn = wave % Tile<T>::WGN;
-#pragma unroll
-  for (int fm = 0; fm < Tile<T>::FM; ++fm)
-#pragma unroll
-    for (int fn = 0; fn < Tile<T>::FN; ++fn)
-#pragma unroll
-      for (int v = 0; v < 16; ++v) acc[fm][fn][v] = 0.f;
+  zero_acc<T>(acc);
   barrier_pinned();   // stage 0 has landed
   Frags<T> f0, f1;
   load_frags<T, false, BK>(f0, stage_ptr(0), stage_ptr(0) + R::A_BYTES, 0, wm, wn);
-  for (int kt = 0; kt < nk; ++kt) {
+  for_each_slice<NS>(nk, f0, f1, [&](int kt, int s, Frags<T>& cur, Frags<T>& nxt) {
     const char* st = stage_ptr(kt);
-#pragma unroll
-    for (int s = 0; s < NS; s += 2) {
-      load_frags<T, false, BK>(f1, st, st + R::A_BYTES, s + 1, wm, wn);
-      mma<T, SWAP>(acc, f0);
-      if (s + 2 < NS) {
-        load_frags<T, false, BK>(f0, st, st + R::A_BYTES, s + 2, wm, wn);
-        mma<T, SWAP>(acc, f1);
-      } else {
-        __builtin_amdgcn_sched_barrier(0);
-        __builtin_amdgcn_s_waitcnt(0xC07F);   // lgkmcnt(0): stage kt is read
-        barrier_pinned();                     // and stage kt + 1 has landed
-        if (kt + 1 < nk) {
-          const char* nxp = stage_ptr(kt + 1);
-          load_frags<T, false, BK>(f0, nxp, nxp + R::A_BYTES, 0, wm, wn);
-        }
-        __builtin_amdgcn_sched_barrier(0);
-        mma<T, SWAP>(acc, f1);
+    if (s + 1 < NS) {
+      load_frags<T, false, BK>(nxt, st, st + R::A_BYTES, s + 1, wm, wn);
+      mma<T, SWAP>(acc, cur);
+    } else {
+      __builtin_amdgcn_sched_barrier(0);
+      __builtin_amdgcn_s_waitcnt(0xC07F);   // lgkmcnt(0): stage kt is read
+      barrier_pinned();                     // and stage kt + 1 has landed
+      if (kt + 1 < nk) {
+        const char* nxp = stage_ptr(kt + 1);
+        load_frags<T, false, BK>(nxt, nxp, nxp + R::A_BYTES, 0, wm, wn);
       }
+      __builtin_amdgcn_sched_barrier(0);
+      mma<T, SWAP>(acc, cur);
     }
-  }
+  });
   return true;
 }
 
-// Ping-pong schedule of the 8-wave tile (mainloop_pp_kc5 below).  Waves 0-3
+// Ping-pong schedule of the 8-wave tile (mainloop_pp below).  Waves 0-3
 // (group 0) and 4-7 (group 1) occupy one slot per SIMD each; group 1 runs
-// one phase behind, so that while one wave of a SIMD issues the 16 MFMAs of
-// a 32-wide K step from registers, the other issues its DMA and reads its
-// operands of the next step from LDS.  Every phase ends
-// with a workgroup barrier:
-//   group 0: [MEM(h) | COMP(h)] for each 32-wide step h, then one idle phase;
-//   group 1: one idle phase, then [MEM(h) | COMP(h)].
-// Stages are 64 K elements wide (two steps), so a K-contiguous row of a
-// stage is one full 128-byte line, which the global -> LDS path moves at
-// twice the rate of 64-byte half lines.  That path takes about 64 bytes per
-// clock and compute unit, so the loop issues one operand stage (32 KB per
-// workgroup) per step rather than a whole stage every other step.  The data
-// a step reads must be in LDS before group 0's MEM of that step: at the end
-// of the step before, group 0 waits for its own DMAs at the end of its COMP,
-// group 1 at the end of its MEM (together with its LDS reads), both before
-// the same barrier.  A buffer is refilled only after the barrier that ends
-// its last reader's MEM phase.  A MEM phase issues its LDS reads before its
-// DMA: issuing a DMA stalls the wave while the compute unit's queue drains,
-// and that stall then overlaps the reads' completion instead of delaying
-// their start.
-
-// Ping-pong loop of the 8-wave tile: operand a K-contiguous rows (of Y for
-// the Gram, of A for the polynomial, of B~ for the update), operand b
-// K-contiguous rows too (RM = false) or the update's K x T row-major block of
-// Y (RM = true).  A stage of K-contiguous rows cannot be split along K
-// without halving its 128-byte row pieces, so instead of two stages the ring
-// holds five operand slots of one operand stage each (the whole 160 KB),
-// filled in the order a(0), b(0), a(1), b(1), ...: operand stage i goes into
-// slot i % 5.  The slot of a(j + 2) is that of b(j - 1) and the slot of
-// b(j + 1) that of a(j - 1), both free once stage j - 1 has been read, so the
-// first step of stage j issues b(j + 1) and the second a(j + 2): one operand
-// stage per step.  At the end of stage j's second step every wave waits for
-// a(j + 1) and b(j + 1), leaving a(j + 2) in flight; five consecutive operand
-// stages are live at most (a(j), b(j) read, a(j + 1), b(j + 1), a(j + 2)).
+// one phase behind, so that while one wave of a SIMD issues the MFMAs of a
+// whole 64-wide K stage from registers, the other reads its operands of the
+// next stage from LDS and issues its group's DMA.  Every phase ends with a
+// workgroup barrier:
+//   group 0: [MEM(j) | COMP(j)] for each stage j, then one idle phase;
+//   group 1: one idle phase, then [MEM(j) | COMP(j)].
+// A COMP phase is 2 slices x FM x FN = 64 v_mfma_f32_16x16x32_bf16 per wave
+// (96 operand registers next to the 128 accumulators), so a stage costs two
+// barriers.  K-contiguous rows of a stage are one full 128-byte line, which
+// the global -> LDS path moves at twice the rate of 64-byte half lines.
+//
+// The LDS holds five operand slots of one operand stage (32 KB) each, the
+// whole 160 KB, filled in the order a(0), b(0), a(1), b(1), ...: operand stage
+// i goes into slot i % 5.  In MEM(j), group 0 issues b(j + 1) into the slot of
+// a(j - 1) and group 1 (one phase later) issues a(j + 2) into the slot of
+// b(j - 1); both slots were read by both groups in MEM(j - 1).  Five operand
+// stages are live at most (a(j), b(j) being read, a(j + 1), b(j + 1),
+// a(j + 2)).  Before the barrier that ends its COMP(j), group 0 waits for its
+// b(j + 1); before the barrier that ends its MEM(j), group 1 waits for its
+// a(j + 1), leaving a(j + 2) in flight: the barrier that opens group 0's
+// MEM(j + 1) comes after both.
 template <int T, bool RM, bool SWAP, int BK>
-__device__ inline void mainloop_pp_kc5(f32x16_t (&acc)[Tile<T>::FM][Tile<T>::FN], char* smem,
-                                       const uint16_t* a, int64_t lda, const uint16_t* b,
-                                       int64_t ldb, int K) {
+__device__ inline void mainloop_pp(AccT<T>& acc, char* smem, const uint16_t* a, int64_t lda,
+                                   const uint16_t* b, int64_t ldb, int K) {
   static_assert(Tile<T>::NW == 8, "ping-pong needs two waves per SIMD");
+  static_assert(BK == 64, "two 32-wide slices per stage");
   using R = Ring<T, BK>;
-  constexpr int DO = R::DMA_OP, SLOTS = 5;
-  static_assert(BK == 64, "two 32-wide steps per stage");
+  constexpr int SLOTS = 5;
+  constexpr int QG = T * BK / 512 / 4;    // 1 KB DMAs per wave of a group and operand stage
   static_assert(SLOTS * R::A_BYTES <= R::LDS, "five operand slots");
   const int wave = threadIdx.x >> 6;
   const int wm = wave / 4, wn = wave % 4;
+  const int w4 = wave & 3;
   const bool g1 = __builtin_amdgcn_readfirstlane(wave) >= 4;
-#pragma unroll
-  for (int fm = 0; fm < Tile<T>::FM; ++fm)
-#pragma unroll
-    for (int fn = 0; fn < Tile<T>::FN; ++fn)
-#pragma unroll
-      for (int v = 0; v < 16; ++v) acc[fm][fn][v] = 0.f;
+  zero_acc<T>(acc);
 
   const uint32_t lds0 = lds_addr(smem);
   const int nk = K / BK;
   auto slot_lds = [&](int i) { return lds0 + uint32_t((i % SLOTS) * R::A_BYTES); };
   auto slot_ptr = [&](int i) { return smem + (i % SLOTS) * R::A_BYTES; };
-  auto issue_a = [&](int kt) { issue_kc<T, BK>(a, lda, kt * BK, slot_lds(2 * kt)); };
-  auto issue_b = [&](int kt) {
-    if constexpr (RM) {
+  // instructions q0 .. q1 - 1 of this wave's share of operand stage a(kt) / b(kt)
+  auto issue_a = [&](int kt, int q0, int q1) {
 #pragma unroll
-      for (int q = 0; q < DO; ++q) dma_rm<T, BK>(b, ldb, kt * BK, slot_lds(2 * kt + 1), q);
-    } else {
-      issue_kc<T, BK>(b, ldb, kt * BK, slot_lds(2 * kt + 1));
+    for (int q = q0; q < q1; ++q) dma_kc_w<T, BK, 4>(a, lda, kt * BK, slot_lds(2 * kt), q, w4);
+  };
+  auto issue_b = [&](int kt, int q0, int q1) {
+#pragma unroll
+    for (int q = q0; q < q1; ++q) {
+      if constexpr (RM) dma_rm_w<T, BK, 4>(b, ldb, kt * BK, slot_lds(2 * kt + 1), q, w4);
+      else dma_kc_w<T, BK, 4>(b, ldb, kt * BK, slot_lds(2 * kt + 1), q, w4);
     }
   };
 
-  issue_a(0);
-  issue_b(0);
-  if (nk > 1) {
-    issue_a(1);
-    __builtin_amdgcn_s_waitcnt(0xC07F);
-    ring_sync_dma<DO>();
+  if (!g1) {
+    issue_b(0, 0, QG);
   } else {
-    __builtin_amdgcn_s_waitcnt(0xC07F);
-    ring_sync_dma<0>();
+    issue_a(0, 0, QG);
+    if (nk > 1) issue_a(1, 0, QG);
   }
+  __builtin_amdgcn_s_waitcnt(0xC07F);
+  ring_sync_dma<0>();
   if (g1) barrier_pinned();
 
   Frags<T> f0, f1;
   for (int j = 0; j < nk; ++j) {
     const char* sa = slot_ptr(2 * j);
     const char* sb = slot_ptr(2 * j + 1);
-#pragma unroll
-    for (int hs = 0; hs < 2; ++hs) {
-      // MEM
-      load_frags<T, RM, BK>(f0, sa, sb, 2 * hs, wm, wn);
-      load_frags<T, RM, BK>(f1, sa, sb, 2 * hs + 1, wm, wn);
-      if (hs == 0) {
-        if (j + 1 < nk) issue_b(j + 1);
-      } else {
-        if (j + 2 < nk) issue_a(j + 2);
-      }
-      if (g1) {
-        __builtin_amdgcn_s_waitcnt(0xC07F);   // lgkmcnt(0)
-        if (hs == 1) {
-          if (j + 2 < nk) dma_wait<DO>();
-          else dma_wait<0>();
-        }
-      }
-      barrier_pinned();
-      // COMP
-      mma<T, SWAP>(acc, f0);
-      mma<T, SWAP>(acc, f1);
-      if (!g1 && hs == 1) {
-        if (j + 2 < nk) dma_wait<DO>();
-        else dma_wait<0>();
-      }
-      barrier_pinned();
+    // MEM: the group's DMA first, then the LDS reads of both slices.  The
+    // two share the LDS (the DMA writes its data there), so they take about
+    // the sum of their times in either order; issued first, the DMA lands
+    // a whole memory phase earlier, which removes most of group 0's wait
+    // for b(j + 1) at the end of its COMP(j).
+    if (!g1) {
+      if (j + 1 < nk) issue_b(j + 1, 0, QG);
+    } else {
+      if (j + 2 < nk) issue_a(j + 2, 0, QG);
     }
+    __builtin_amdgcn_sched_barrier(0);
+    load_frags<T, RM, BK>(f0, sa, sb, 0, wm, wn);
+    load_frags<T, RM, BK>(f1, sa, sb, 1, wm, wn);
+    __builtin_amdgcn_s_waitcnt(0xC07F);   // lgkmcnt(0)
+    if (g1) {
+      if (j + 2 < nk) dma_wait<QG>();
+      else dma_wait<0>();
+    }
+    barrier_pinned();
+    // COMP
+    mma<T, SWAP>(acc, f0);
+    mma<T, SWAP>(acc, f1);
+    if (!g1) dma_wait<0>();
+    barrier_pinned();
   }
   if (!g1) barrier_pinned();
   __builtin_amdgcn_s_waitcnt(0xC07F);
@@ -617,11 +654,10 @@ __device__ inline void mainloop_pp_kc5(f32x16_t (&acc)[Tile<T>::FM][Tile<T>::FN]
 
 template <int T, bool RM, bool SWAP, int BK>
 // Returns false in the producer waves, which then leave the kernel.
-__device__ inline bool run_mainloop(f32x16_t (&acc)[Tile<T>::FM][Tile<T>::FN], char* smem,
-                                    const uint16_t* a, int64_t lda, const uint16_t* b,
-                                    int64_t ldb, int K) {
+__device__ inline bool run_mainloop(AccT<T>& acc, char* smem, const uint16_t* a, int64_t lda,
+                                    const uint16_t* b, int64_t ldb, int K) {
   if constexpr (Tile<T>::NW == 8) {
-    mainloop_pp_kc5<T, RM, SWAP, BK>(acc, smem, a, lda, b, ldb, K);
+    mainloop_pp<T, RM, SWAP, BK>(acc, smem, a, lda, b, ldb, K);
     return true;
   } else if constexpr (RM) {   // the update's smaller tiles: compute waves issue the DMA
     mainloop<T, RM, SWAP, BK>(acc, smem, a, lda, b, ldb, K);
@@ -728,13 +764,15 @@ __device__ inline bool sym_tile(const Phase& P, Loc& L, int& I, int& J) {
   return true;
 }
 
+// First of the 4 consecutive rows, and the column, of this lane's elements of
+// accumulator block (fm, fn) (operands not swapped).
 template <int T>
-__device__ inline int acc_row(int wm, int fm, int v) {
-  return wm * Tile<T>::TWM + fm * 32 + 8 * (v >> 2) + 4 * ((threadIdx.x & 63) >> 5) + (v & 3);
+__device__ inline int acc_row(int wm, int fm) {
+  return wm * Tile<T>::TWM + fm * 16 + 4 * ((threadIdx.x & 63) >> 4);
 }
 template <int T>
 __device__ inline int acc_col(int wn, int fn) {
-  return wn * Tile<T>::TWN + fn * 32 + (threadIdx.x & 31);
+  return wn * Tile<T>::TWN + fn * 16 + (threadIdx.x & 15);
 }
 __device__ inline int wave_m(int wgn) { return int(threadIdx.x >> 6) / wgn; }
 __device__ inline int wave_n(int wgn) { return int(threadIdx.x >> 6) % wgn; }
@@ -862,26 +900,25 @@ __device__ inline void load_rows(char* st, const uint16_t* src, int64_t ld, int6
 // (j, i); the stage then holds tile (J, I), stored as rows of block J and,
 // off the diagonal, transposed as tile (I, J).  `staged` is the stage's
 // previous bf16 at that position (the polynomial preloads A's tile (J, I)).
+// Each lane's 4 elements of a block are consecutive rows of one column: one
+// 8-byte stage row piece.
 template <int T, class Fv>
-__device__ inline void epilogue_sym(const f32x16_t (&acc)[Tile<T>::FM][Tile<T>::FN], char* st,
-                                    uint16_t* D, int64_t ld, int I, int J, Fv f) {
+__device__ inline void epilogue_sym(const AccT<T>& acc, char* st, uint16_t* D, int64_t ld, int I,
+                                    int J, Fv f) {
   const int wm = wave_m(Tile<T>::WGN), wn = wave_n(Tile<T>::WGN);
 #pragma unroll
   for (int fm = 0; fm < Tile<T>::FM; ++fm)
 #pragma unroll
     for (int fn = 0; fn < Tile<T>::FN; ++fn) {
       const int c = acc_col<T>(wn, fn);
+      const int r0 = acc_row<T>(wm, fm);
+      char* p = st + c * Stage<T>::RS + r0 * 2;
+      const uint2 old = *reinterpret_cast<const uint2*>(p);
+      const uint16_t* o = reinterpret_cast<const uint16_t*>(&old);
+      uint16_t out[4];
 #pragma unroll
-      for (int v4 = 0; v4 < 4; ++v4) {
-        const int r0 = acc_row<T>(wm, fm, 4 * v4);
-        char* p = st + c * Stage<T>::RS + r0 * 2;
-        const uint2 old = *reinterpret_cast<const uint2*>(p);
-        const uint16_t* o = reinterpret_cast<const uint16_t*>(&old);
-        uint16_t out[4];
-#pragma unroll
-        for (int u = 0; u < 4; ++u) out[u] = f2bf(f(r0 + u, c, acc[fm][fn][4 * v4 + u], o[u]));
-        *reinterpret_cast<uint2*>(p) = *reinterpret_cast<const uint2*>(out);
-      }
+      for (int u = 0; u < 4; ++u) out[u] = f2bf(f(r0 + u, c, acc[fm][fn][u], o[u]));
+      *reinterpret_cast<uint2*>(p) = *reinterpret_cast<const uint2*>(out);
     }
   __syncthreads();
   store_rows<T>(st, D, ld, int64_t(J) * T, int64_t(I) * T);
@@ -895,40 +932,32 @@ __device__ inline void epilogue_sym(const f32x16_t (&acc)[Tile<T>::FM][Tile<T>::
 // the first goes through the stage while the second waits in registers as
 // packed bf16, then takes the stage in a second pass.
 template <int T, class Fv>
-__device__ inline void epilogue_sym_scaled(const f32x16_t (&acc)[Tile<T>::FM][Tile<T>::FN],
-                                           char* st, uint16_t* D, int64_t ld, int I, int J, Fv f,
-                                           const float* __restrict__ s) {
+__device__ inline void epilogue_sym_scaled(const AccT<T>& acc, char* st, uint16_t* D, int64_t ld,
+                                           int I, int J, Fv f, const float* __restrict__ s) {
   constexpr int FM = Tile<T>::FM, FN = Tile<T>::FN;
   const int wm = wave_m(Tile<T>::WGN), wn = wave_n(Tile<T>::WGN);
-  uint2 keep[FM][FN][4];
+  uint2 keep[FM][FN];
 #pragma unroll
   for (int fm = 0; fm < FM; ++fm) {
-    // s of this lane's 16 rows of the 32-row block fm (4 runs of 4 rows)
-    float4 si[4];
-#pragma unroll
-    for (int v4 = 0; v4 < 4; ++v4)
-      si[v4] = *reinterpret_cast<const float4*>(s + I * T + acc_row<T>(wm, fm, 4 * v4));
+    const int r0 = acc_row<T>(wm, fm);
+    const float4 si = *reinterpret_cast<const float4*>(s + I * T + r0);   // s of the 4 rows
+    const float sv[4] = {si.x, si.y, si.z, si.w};
 #pragma unroll
     for (int fn = 0; fn < FN; ++fn) {
       const int c = acc_col<T>(wn, fn);
       const float sj = s[J * T + c];
+      char* p = st + c * Stage<T>::RS + r0 * 2;
+      const uint2 old = *reinterpret_cast<const uint2*>(p);
+      const uint16_t* o = reinterpret_cast<const uint16_t*>(&old);
+      uint16_t out[4], out2[4];
 #pragma unroll
-      for (int v4 = 0; v4 < 4; ++v4) {
-        const int r0 = acc_row<T>(wm, fm, 4 * v4);
-        char* p = st + c * Stage<T>::RS + r0 * 2;
-        const uint2 old = *reinterpret_cast<const uint2*>(p);
-        const uint16_t* o = reinterpret_cast<const uint16_t*>(&old);
-        const float sv[4] = {si[v4].x, si[v4].y, si[v4].z, si[v4].w};
-        uint16_t out[4], out2[4];
-#pragma unroll
-        for (int u = 0; u < 4; ++u) {
-          const float x = f(r0 + u, c, acc[fm][fn][4 * v4 + u], o[u]);
-          out[u] = f2bf(x * sv[u]);
-          out2[u] = f2bf(x * sj);
-        }
-        *reinterpret_cast<uint2*>(p) = *reinterpret_cast<const uint2*>(out);
-        keep[fm][fn][v4] = *reinterpret_cast<const uint2*>(out2);
+      for (int u = 0; u < 4; ++u) {
+        const float x = f(r0 + u, c, acc[fm][fn][u], o[u]);
+        out[u] = f2bf(x * sv[u]);
+        out2[u] = f2bf(x * sj);
       }
+      *reinterpret_cast<uint2*>(p) = *reinterpret_cast<const uint2*>(out);
+      keep[fm][fn] = *reinterpret_cast<const uint2*>(out2);
     }
     __builtin_amdgcn_sched_barrier(0);   // keeps the loads of the next block here
   }
@@ -939,13 +968,9 @@ __device__ inline void epilogue_sym_scaled(const f32x16_t (&acc)[Tile<T>::FM][Ti
 #pragma unroll
   for (int fm = 0; fm < FM; ++fm)
 #pragma unroll
-    for (int fn = 0; fn < FN; ++fn) {
-      const int c = acc_col<T>(wn, fn);
-#pragma unroll
-      for (int v4 = 0; v4 < 4; ++v4)
-        *reinterpret_cast<uint2*>(st + c * Stage<T>::RS + acc_row<T>(wm, fm, 4 * v4) * 2) =
-            keep[fm][fn][v4];
-    }
+    for (int fn = 0; fn < FN; ++fn)
+      *reinterpret_cast<uint2*>(st + acc_col<T>(wn, fn) * Stage<T>::RS + acc_row<T>(wm, fm) * 2) =
+          keep[fm][fn];
   __syncthreads();
   store_cols<T>(st, D, ld, int64_t(I) * T, int64_t(J) * T);   // C[i][j]
 }
@@ -953,24 +978,16 @@ __device__ inline void epilogue_sym_scaled(const f32x16_t (&acc)[Tile<T>::FM][Ti
 // fp32 store of an upper tile straight from the registers (first Gram only;
 // k_apply_s reads the upper tiles and writes both halves of A1).
 template <int T>
-__device__ inline void store_sym_f32(const f32x16_t (&acc)[Tile<T>::FM][Tile<T>::FN], float* D,
-                                     int64_t ld, int I, int J) {
+__device__ inline void store_sym_f32(const AccT<T>& acc, float* D, int64_t ld, int I, int J) {
   const int wm = wave_m(Tile<T>::WGN), wn = wave_n(Tile<T>::WGN);
 #pragma unroll
   for (int fm = 0; fm < Tile<T>::FM; ++fm)
 #pragma unroll
     for (int fn = 0; fn < Tile<T>::FN; ++fn) {
       const int j = J * T + acc_col<T>(wn, fn);
+      const int ib = I * T + acc_row<T>(wm, fm);
 #pragma unroll
-      for (int v4 = 0; v4 < 4; ++v4) {
-        const int ib = I * T + acc_row<T>(wm, fm, 4 * v4);
-        float m[4];
-#pragma unroll
-        for (int u = 0; u < 4; ++u) {
-          m[u] = acc[fm][fn][4 * v4 + u];
-          D[int64_t(ib + u) * ld + j] = m[u];
-        }
-      }
+      for (int u = 0; u < 4; ++u) D[int64_t(ib + u) * ld + j] = acc[fm][fn][u];
     }
 }
 
@@ -988,7 +1005,7 @@ __global__ __launch_bounds__(Tile<T>::NTT) void k_gram_fast(const Phase P) {
   char* w = ws_of(P, E, L.mat);
   const WsLayout WL = ws_layout(E.kp, E.Np, 2);
   const int64_t ldy = WL.ldy;
-  f32x16_t acc[FM][FN];
+  AccT<T> acc;
   if (!run_mainloop<T, false, false, BK>(acc, smem, Y + int64_t(I) * T * ldy, ldy, Y + int64_t(J) * T * ldy, ldy, Np)) return;
 
   if (P.flags & kA32) {
@@ -1003,53 +1020,52 @@ __global__ __launch_bounds__(Tile<T>::NTT) void k_gram_fast(const Phase P) {
     // part[b][i] = sum over the 64 columns of block b of |A0_ij| (with kRowSq:
     // A0_ij^2, whose total is ||A0||_F^2 for the Schatten-4 scale), from the fp32
     // accumulators.  The reduction tree is fixed for every tile size: each
-    // 32 x 32 MFMA block is reduced first (a butterfly over its 32 columns for
-    // the row sums, the same pairing over its 32 rows for the column sums),
-    // then two adjacent 32-blocks are added.  Off-diagonal tiles also emit the
-    // partials of the mirrored tile (column sums), so every row of A0 gets
-    // kp / 64 partials, identical whichever tile size produced them.
+    // 16 x 16 MFMA block is reduced first, pairing column (row) index bits 0,
+    // 1, 2, 3 in that order for the row (column) sums, then the four 16-blocks
+    // of a 64-column block are added as (b0 + b1) + (b2 + b3).  Off-diagonal
+    // tiles also emit the partials of the mirrored tile (column sums, bit for
+    // bit the row sums of the transposed block, which a smaller tile size may
+    // compute as row sums), so every row of A0 gets kp / 64 partials,
+    // identical whichever tile size produced them.
     __syncthreads();
     float* part = reinterpret_cast<float*>(w + WL.part);
     const bool sq = (P.flags & kRowSq) != 0u;   // Schatten-4: sums of A0_ij^2
     auto mag = [sq](float x) { return sq ? x * x : fabsf(x); };
-    constexpr int NB = T / 32;
-    float* rs = reinterpret_cast<float*>(smem);       // [NB][T] row sums over 32-column blocks
-    float* cs = rs + NB * T;                          // [NB][T] column sums over 32-row blocks
+    constexpr int NB = T / 16;
+    float* rs = reinterpret_cast<float*>(smem);       // [NB][T] row sums over 16-column blocks
+    float* cs = rs + NB * T;                          // [NB][T] column sums over 16-row blocks
     const int lane = threadIdx.x & 63;
     const int wm = wave_m(Tile<T>::WGN), wn = wave_n(Tile<T>::WGN);
 #pragma unroll
     for (int fm = 0; fm < FM; ++fm)
 #pragma unroll
       for (int fn = 0; fn < FN; ++fn) {
+        // row sums: lanes 16 g .. 16 g + 15 hold the 16 columns of rows
+        // 4 g + v; butterfly over lane bits 0..3
 #pragma unroll
-        for (int v = 0; v < 16; ++v) {
+        for (int v = 0; v < 4; ++v) {
           float x = mag(acc[fm][fn][v]);
 #pragma unroll
-          for (int off = 16; off >= 1; off >>= 1) x += __shfl_xor(x, off, 64);
-          if ((lane & 31) == 0) rs[((wn * Tile<T>::TWN) / 32 + fn) * T + acc_row<T>(wm, fm, v)] = x;
+          for (int off = 1; off <= 8; off <<= 1) x += __shfl_xor(x, off, 64);
+          if ((lane & 15) == 0) rs[((wn * Tile<T>::TWN) / 16 + fn) * T + acc_row<T>(wm, fm) + v] = x;
         }
-        // Column sums with the pairing of the row butterfly above, applied to
-        // the row index 8 (v / 4) + 4 (lane / 32) + v % 4: bit 4 (v ^ 8),
-        // bit 3 (v ^ 4), bit 2 (the other lane half), bit 1, bit 0.  A column
-        // sum is then bit for bit the row sum of the transposed block, which
-        // the mirrored tile of a smaller tile size computes as a row sum.
-        float y[8];
-#pragma unroll
-        for (int v = 0; v < 8; ++v) y[v] = mag(acc[fm][fn][v]) + mag(acc[fm][fn][v + 8]);
-#pragma unroll
-        for (int v = 0; v < 4; ++v) y[v] += y[v + 4];
-#pragma unroll
-        for (int v = 0; v < 4; ++v) y[v] += __shfl_xor(y[v], 32, 64);
-        const float col = (y[0] + y[2]) + (y[1] + y[3]);
-        if (lane < 32) cs[((wm * Tile<T>::TWM) / 32 + fm) * T + acc_col<T>(wn, fn)] = col;
+        // column sums: row bits 0, 1 are v's, bits 2, 3 the lane's bits 4, 5
+        const float y = (mag(acc[fm][fn][0]) + mag(acc[fm][fn][1])) +
+                        (mag(acc[fm][fn][2]) + mag(acc[fm][fn][3]));
+        float col = y + __shfl_xor(y, 16, 64);
+        col += __shfl_xor(col, 32, 64);
+        if (lane < 16) cs[((wm * Tile<T>::TWM) / 16 + fm) * T + acc_col<T>(wn, fn)] = col;
       }
     __syncthreads();
     constexpr int NB64 = T / 64;
     for (int q = threadIdx.x; q < NB64 * T; q += Tile<T>::NT) {
       const int b = q / T, r = q - b * T;
-      part[int64_t(J * NB64 + b) * kp + I * T + r] = rs[(2 * b) * T + r] + rs[(2 * b + 1) * T + r];
-      if (I != J)
-        part[int64_t(I * NB64 + b) * kp + J * T + r] = cs[(2 * b) * T + r] + cs[(2 * b + 1) * T + r];
+      const float* x = rs + (4 * b) * T + r;
+      part[int64_t(J * NB64 + b) * kp + I * T + r] = (x[0] + x[T]) + (x[2 * T] + x[3 * T]);
+      if (I != J) {
+        const float* y = cs + (4 * b) * T + r;
+        part[int64_t(I * NB64 + b) * kp + J * T + r] = (y[0] + y[T]) + (y[2 * T] + y[3 * T]);
+      }
     }
   }
 }
@@ -1070,7 +1086,7 @@ __global__ __launch_bounds__(Tile<T>::NTT) void k_poly_fast(const Phase P) {
   const uint16_t* A = reinterpret_cast<const uint16_t*>(w + WL.a);
   uint16_t* B = reinterpret_cast<uint16_t*>(w + WL.b);
   const int64_t ldg = WL.ldg;
-  f32x16_t acc[FM][FN];
+  AccT<T> acc;
   if (!run_mainloop<T, false, false, BK>(acc, smem, A + int64_t(I) * T * ldg, ldg, A + int64_t(J) * T * ldg, ldg, kp)) return;
   load_rows<T>(smem, A, ldg, int64_t(J) * T, int64_t(I) * T);
   __syncthreads();
@@ -1120,26 +1136,24 @@ __global__ __launch_bounds__(Tile<T>::NT) void k_update_fast(const Phase P) {
   const uint16_t* B = reinterpret_cast<const uint16_t*>(w + WL.b);
   const uint16_t* Y = wbuf(P, E, L.mat, P.src);
   const int64_t ldg = WL.ldg, ldy = WL.ldy;
-  f32x16_t acc[FM][FN];
+  AccT<T> acc;
   run_mainloop<T, true, true, BK>(acc, smem, B + int64_t(I) * T * ldg, ldg, Y + int64_t(Lb) * T, ldy, kp);
 
-  // acc[fm][fn] element v: output row i = wm*TWM + fm*32 + lane%32, columns
-  // l0..l0+3 with l0 = wn*TWN + fn*32 + 8(v/4) + 4(lane/32)
+  // acc[fm][fn] element u: output row i = wm*TWM + fm*16 + lane%16, column
+  // l0 + u with l0 = 16 (fn WGN + wn) + 4(lane/16) (the waves' column blocks
+  // interleave, as the operand reads of the row-major Y stage assign them)
   const int lane = threadIdx.x & 63;
   const int wm = wave_m(Tile<T>::WGN), wn = wave_n(Tile<T>::WGN);
 #pragma unroll
   for (int fm = 0; fm < FM; ++fm)
 #pragma unroll
     for (int fn = 0; fn < FN; ++fn) {
-      const int i = wm * Tile<T>::TWM + fm * 32 + (lane & 31);
+      const int i = wm * Tile<T>::TWM + fm * 16 + (lane & 15);
+      const int l0 = 16 * (fn * Tile<T>::WGN + wn) + 4 * (lane >> 4);
+      uint16_t out[4];
 #pragma unroll
-      for (int v4 = 0; v4 < 4; ++v4) {
-        const int l0 = wn * Tile<T>::TWN + fn * 32 + 8 * v4 + 4 * (lane >> 5);
-        uint16_t out[4];
-#pragma unroll
-        for (int u = 0; u < 4; ++u) out[u] = f2bf(acc[fm][fn][4 * v4 + u]);
-        *reinterpret_cast<uint2*>(smem + i * Stage<T>::RS + l0 * 2) = *reinterpret_cast<const uint2*>(out);
-      }
+      for (int u = 0; u < 4; ++u) out[u] = f2bf(acc[fm][fn][u]);
+      *reinterpret_cast<uint2*>(smem + i * Stage<T>::RS + l0 * 2) = *reinterpret_cast<const uint2*>(out);
     }
   __syncthreads();
   if (P.dst != kSlotFinal)
