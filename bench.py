@@ -66,6 +66,9 @@ def main(argv=None) -> int:
                     help="time the optimizer step (tm_muon_step_grouped: momentum, bf16 "
                          "orthogonalization, fp32 parameter update) over the workload's matrices "
                          "instead of the orthogonalization alone")
+    ap.add_argument("--no-configs", action="store_true",
+                    help="skip the per-configuration sub-records that follow the default "
+                         "workload's line (every other synthetic workload, timed the same way)")
     ap.add_argument("--inputs", default="powerlaw", choices=["powerlaw", "gaussian"],
                     help="powerlaw: the seeded power-law-plus-noise recipe (QR on the GPU); "
                          "gaussian: i.i.d. N(0,1) entries, the paper's own synthetic law "
@@ -215,12 +218,16 @@ def main(argv=None) -> int:
         "tflops_algorithmic": round(tflops, 2),
         "pct_peak": round(100 * tflops / peak, 2),
         "phase_ms_per_step": {p: round(v[0] / args.steps, 4) for p, v in phases.items()},
-        "roofline": {"bound": "mfma", "kernel": "k_update",
+        "roofline": {"bound": "mfma", "kernel": "k_update_fast",
                      "achieved": round(upd_tflops, 2) if upd_n else None, "peak": peak,
                      "unit": "TFLOP/s", "frac": round(upd_tflops / peak, 4) if upd_n else None,
                      "traffic": None,
                      "launch_avg_ms": round(upd_avg_ms, 4) if upd_n else None,
-                     "flops_per_launch": upd_flops_per_launch},
+                     "launches": upd_n,
+                     "flops_per_launch": upd_flops_per_launch,
+                     "source": "HIP events recorded on the call's stream around every "
+                               "k_update_fast launch of the timed steps (library timing hooks); "
+                               "achieved = update flops of those launches / their summed time"},
     }
 
     if not args.no_cpu_baseline:
@@ -269,11 +276,115 @@ def main(argv=None) -> int:
         torch.cuda.synchronize()
         result["copy_calibration_bytes"] = nbytes
 
+    if not args.no_configs and args.workload == DEFAULT_WORKLOAD and not args.graph:
+        result["configs"] = _config_records(args, dev, progress)
+
     traffic = _recorded_traffic(upd_flops_per_launch) if args.workload == DEFAULT_WORKLOAD else None
     if traffic is not None:
         result["roofline"]["traffic"] = traffic
     print(json.dumps(result), flush=True)
     return 0
+
+
+# The other configurations of the benchmark's workload list, reported as
+# sub-records of the default line: (label, workload, iters, precond).  The
+# 4096 x 14336 half of the 8B-class configuration is the line itself.
+CONFIGS = [
+    ("c1", "single_256_f32", 4, "aol"),
+    ("c2", "gpt2_mlp_768x3072", 4, "aol"),
+    ("c2_muon", "gpt2_mlp_768x3072", 5, "frobenius"),
+    ("c3", "gpt2_small_12layer", 4, "aol"),
+    ("c4_4096x4096", "llm8b_4096x4096_b8", 4, "aol"),
+    ("c5", "resnet_conv_64", 4, "aol"),
+]
+
+
+def _config_records(args, dev, progress):
+    """Each configuration timed like the line (inputs resident in HBM, warm-up,
+    then 20 timed calls on the current stream) but without the per-launch
+    timing hooks, whose two event records per launch matter for the small
+    workloads.  The oracle on matrix 0 of every shape of a configuration, on
+    the host cores, is that configuration's CPU baseline and its parity
+    figure (skipped with --no-cpu-baseline)."""
+    import numpy as np
+    import torch
+
+    from paper_2512_04632_amd import _lib as tm
+    from paper_2512_04632_amd import synth
+
+    out = []
+    steps, warmup = 20, 5
+    stream = torch.cuda.current_stream(dev)
+    for label, wl, iters, precond in CONFIGS:
+        spec = synth.WORKLOADS[wl]
+        dtype = spec["dtype"]
+        tdtype = torch.bfloat16 if dtype == "bf16" else torch.float32
+        entries = spec["entries"]
+        progress(f"config {label}: {wl} {precond} t={iters}")
+        batches = [synth.power_law_batch_device(c, m, n, a, seed=e, device=dev, dtype=tdtype)
+                   for e, (c, m, n, a) in enumerate(entries)]
+        grouped = len(entries) > 1
+
+        def run(bs):
+            if grouped:
+                tm.orthogonalize_grouped([X[i] for X in bs for i in range(X.shape[0])], iters,
+                                         None, precond)
+            else:
+                tm.orthogonalize(bs[0], iters, None, precond)
+
+        hosts = [X[0].float().cpu().numpy().astype(np.float64) for X in batches]
+        clones = [X.clone() for X in batches]
+        run(clones)
+        torch.cuda.synchronize()
+        outs = [X[0].float().cpu().numpy().astype(np.float64) for X in clones]
+        del clones
+        for _ in range(warmup):
+            run(batches)
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(steps):
+            run(batches)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1) / steps
+        n_mat = sum(c for c, _, _, _ in entries)
+        flops = sum(alg_flops(min(m, n), max(m, n), iters)["total"] * c for c, m, n, _ in entries)
+        peak = PEAK_BF16_TFLOPS if dtype == "bf16" else PEAK_F32_TFLOPS
+        rec = {"config": label, "workload": wl, "call": "grouped" if grouped else "batched",
+               "shapes": [[c, m, n] for c, m, n, _ in entries], "dtype": dtype, "iters": iters,
+               "precond": precond, "steps": steps, "ms_per_step": round(ms, 4),
+               "matrices_per_s": round(n_mat / (ms * 1e-3), 2),
+               "tflops_algorithmic": round(flops / (ms * 1e-3) / 1e12, 2),
+               "pct_peak": round(100 * flops / (ms * 1e-3) / 1e12 / peak, 2)}
+        if not args.no_cpu_baseline:
+            # cpu_baseline leg of this configuration: the oracle on matrix 0 of
+            # every shape, timed on the host cores; its results give the parity
+            from oracle import turbomuon as O
+            par, spent = [], 0.0
+            for e, (Xh, G) in enumerate(zip(hosts, outs)):
+                t0 = time.perf_counter()
+                R = O.orthogonalize(Xh, iters, None, precond)
+                spent += time.perf_counter() - t0
+                item = {"entry": e, "matrix": 0,
+                        "rel_frobenius_vs_oracle": float(O.rel_frobenius(G, R)),
+                        "eps_ortho_gpu": float(O.eps_ortho(G)),
+                        "eps_ortho_oracle": float(O.eps_ortho(R))}
+                if label == "c1":   # the accuracy configuration: distance to the SVD polar factor
+                    Q = O.polar_factor(Xh)
+                    item["eps_polar_gpu"] = float(O.eps_polar(G, Xh, Q))
+                    item["eps_polar_oracle"] = float(O.eps_polar(R, Xh, Q))
+                par.append(item)
+            rec["parity"] = par
+            rec["cpu_baseline"] = {"value": round(len(hosts) / spent, 4), "unit": "matrices/s",
+                                   "kind": "oracle",
+                                   "sample": f"matrix 0 of each of the {len(hosts)} shapes, "
+                                             f"fp64 NumPy, {spent:.2f} s"}
+        out.append(rec)
+        del batches
+        torch.cuda.empty_cache()
+    tm.release_workspaces()
+    return out
 
 
 def _bench_optimizer(args, batches, entries, dev, stream, progress):
