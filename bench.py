@@ -296,6 +296,7 @@ CONFIGS = [
     ("c3", "gpt2_small_12layer", 4, "aol"),
     ("c4_4096x4096", "llm8b_4096x4096_b8", 4, "aol"),
     ("c5", "resnet_conv_64", 4, "aol"),
+    ("c5_64x576", "resnet_conv_64x576_b16", 4, "aol"),
 ]
 
 
@@ -348,6 +349,29 @@ def _config_records(args, dev, progress):
         e1.record(stream)
         torch.cuda.synchronize()
         ms = e0.elapsed_time(e1) / steps
+        # calls that the fused small-matrix kernel serves: the same calls on the
+        # tiled kernels, for comparison
+        tm.timing_reset()
+        tm.timing_enable(True)
+        run(batches)
+        torch.cuda.synchronize()
+        tm.timing_enable(False)
+        fused = tm.timing_read("fused")[1] > 0
+        tm.timing_reset()
+        tiled_ms = None
+        if fused:
+            os.environ["TM_DISABLE_FUSED"] = "1"
+            try:
+                for _ in range(warmup):
+                    run(batches)
+                e0.record(stream)
+                for _ in range(steps):
+                    run(batches)
+                e1.record(stream)
+                torch.cuda.synchronize()
+                tiled_ms = e0.elapsed_time(e1) / steps
+            finally:
+                del os.environ["TM_DISABLE_FUSED"]
         n_mat = sum(c for c, _, _, _ in entries)
         flops = sum(alg_flops(min(m, n), max(m, n), iters)["total"] * c for c, m, n, _ in entries)
         peak = PEAK_BF16_TFLOPS if dtype == "bf16" else PEAK_F32_TFLOPS
@@ -356,7 +380,10 @@ def _config_records(args, dev, progress):
                "precond": precond, "steps": steps, "ms_per_step": round(ms, 4),
                "matrices_per_s": round(n_mat / (ms * 1e-3), 2),
                "tflops_algorithmic": round(flops / (ms * 1e-3) / 1e12, 2),
-               "pct_peak": round(100 * flops / (ms * 1e-3) / 1e12 / peak, 2)}
+               "pct_peak": round(100 * flops / (ms * 1e-3) / 1e12 / peak, 2),
+               "kernels": "fused" if fused else "tiled"}
+        if tiled_ms is not None:
+            rec["tiled_ms_per_step"] = round(tiled_ms, 4)
         if not args.no_cpu_baseline:
             # cpu_baseline leg of this configuration: the oracle on matrix 0 of
             # every shape, timed on the host cores; its results give the parity

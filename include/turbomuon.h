@@ -24,6 +24,14 @@
  * AOL row sums are taken from the fp32 Gram accumulators.  f32 entry points
  * store and multiply in fp32.  Results are deterministic: no float atomics.
  *
+ * Small matrices.  A bf16 call with iters >= 1 whose every matrix has
+ * min(m, n) <= 128 and fits, zero padded to multiples of 32, in one compute
+ * unit's 160 KB of LDS (min(m, n) = 64: max(m, n) <= 1088; 128: <= 320) runs
+ * as a single launch, one workgroup per matrix, with no workspace.  Its
+ * results are bit for bit those of the tiled kernels that other calls use
+ * (the same products in the same order, the same roundings); setting
+ * TM_DISABLE_FUSED in the environment sends such calls to the tiled kernels.
+ *
  * Streams and memory.  All work is enqueued on `stream` (a hipStream_t passed
  * as void*, NULL = the legacy default stream) without host synchronisation;
  * results are valid once the stream has passed the call.  Matrix pointers are
@@ -198,7 +206,8 @@ tm_status tm_orthogonalize_noalloc(void* X, int64_t m, int64_t n, int64_t batch,
                                    const float* coeffs, int precond, void* stream);
 
 /* Bytes of workspace a call with these shapes needs (0 on invalid shapes).
- * dtype_bytes is 2 (bf16) or 4 (fp32). */
+ * dtype_bytes is 2 (bf16) or 4 (fp32).  An upper bound: a bf16 call that the
+ * fused small-matrix kernel serves uses none. */
 uint64_t tm_workspace_bytes(const int64_t* m, const int64_t* n, int64_t count,
                             int dtype_bytes);
 
@@ -220,7 +229,8 @@ tm_status tm_release_workspaces(void);
                                     polynomial keeps B~ diag(s) and the update reads X0) */
 #define TM_PHASE_OPT_MOMENTUM 10  /* optimizer step: momentum and the bf16 matrix to orthogonalize */
 #define TM_PHASE_OPT_APPLY    11  /* optimizer step: parameter update */
-#define TM_NUM_PHASES         12
+#define TM_PHASE_FUSED        12  /* bf16 calls of small matrices: every iteration in one launch */
+#define TM_NUM_PHASES         13
 
 /* Timing hooks (a profiling aid for benchmarks).  While enabled, every kernel
  * launch of later calls is bracketed by a pair of HIP events recorded on the

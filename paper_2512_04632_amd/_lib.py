@@ -24,7 +24,7 @@ TM_ERR_HIP = -4
 PRECOND = {"none": 0, "frobenius": 1, "frob": 1, "aol": 2, "schatten4": 3, "s4": 3}
 PHASES = {"transpose_in": 0, "frob": 1, "gram": 2, "aol_vector": 3, "poly": 4, "update": 5,
           "apply_scale": 6, "copy_out": 7, "load_in": 8, "scale_a": 9, "opt_momentum": 10,
-          "opt_apply": 11}
+          "opt_apply": 11, "fused": 12}
 TM_MAX_DIM = 65536
 TM_MAX_ITERS = 64
 

@@ -49,6 +49,7 @@ def build(verbose: bool = False) -> str:
             (os.path.join(CSRC, "tm_fast.hip"), [], "k_fast.o"),
             (os.path.join(CSRC, "tm_optim.hip"), [], "k_optim.o"),
             (os.path.join(CSRC, "tm_noalloc.hip"), [], "noalloc.o"),
+            (os.path.join(CSRC, "tm_small.hip"), [], "k_small.o"),
             (os.path.join(CSRC, "tm_api.cpp"), [], "api.o"),
         ]
         cmds = [[HIPCC] + COMMON + extra + ["-c", src, "-o", os.path.join(tmp, obj)]

@@ -23,6 +23,7 @@ hipError_t launch_elementwise_bf16(int kind, const Phase& P, hipStream_t st);
 hipError_t launch_fast_bf16(int kind, int cfg, int step, const Phase& P, hipStream_t st);
 hipError_t launch_phase_f32(int kind, int cfg, const Phase& P, hipStream_t st);
 hipError_t launch_opt(int apply, const OptPhase& P, hipStream_t st);
+hipError_t launch_small_bf16(int F, int big, const SmallPhase& P, hipStream_t st);
 }  // namespace tmk
 
 namespace {
@@ -421,6 +422,91 @@ tm_status launch(const Plan& pl, int kind, int cfg, int src, int dst, float a, f
   return TM_OK;
 }
 
+// Fused small-matrix path (bf16): a matrix qualifies when k <= 128 and its
+// padded Y, A and B fit in the 160 KB of LDS of one compute unit.
+constexpr uint64_t kSmallLdsBig = 160u * 1024u;   // variants of the fused kernel
+constexpr uint64_t kSmallLdsLow = 64u * 1024u;    // (two workgroups per compute unit)
+
+bool small_eligible(const Item& it) {
+  return it.k <= uint32_t(tmk::kSmallMaxK) && tmk::small_lds_bytes(it.k, it.N) <= kSmallLdsBig;
+}
+
+// Every iteration of every matrix in one launch per (kp / 32, LDS variant)
+// class and per chunk of kMaxSmallEntries entries / kMaxSmallPtrs pointers;
+// consecutive single matrices of one shape share a kPtrTab entry.  No
+// workspace: everything between reading X and writing the result stays in LDS.
+tm_status plan_small(const Plan& pl, int iters, const float* coeffs, int precond) {
+  const std::vector<Item>& items = *pl.items;
+  for (int F = 1; F <= tmk::kSmallMaxK / 32; ++F)
+    for (int big = 0; big < 2; ++big) {
+      std::vector<size_t> idx;
+      for (size_t i = 0; i < items.size(); ++i) {
+        const Item& it = items[i];
+        if (int(tmk::small_kp(it.k) / 32u) == F &&
+            int(tmk::small_lds_bytes(it.k, it.N) > kSmallLdsLow) == big)
+          idx.push_back(i);
+      }
+      size_t i = 0;
+      while (i < idx.size()) {
+        tmk::SmallPhase P;
+        std::memset(&P, 0, sizeof(P));
+        P.iters = iters;
+        P.precond = precond;
+        for (int t = 0; t < iters; ++t) {
+          P.coef[t][0] = coeffs ? coeffs[3 * t] : kA;
+          P.coef[t][1] = coeffs ? coeffs[3 * t + 1] : kB;
+          P.coef[t][2] = coeffs ? coeffs[3 * t + 2] : kC;
+        }
+        uint64_t start = 0;
+        int xp = 0;
+        while (i < idx.size() && P.nent < tmk::kMaxSmallEntries) {
+          const Item& it = items[idx[i]];
+          Entry& E = P.e[P.nent];
+          E.x = it.x;
+          E.k = it.k;
+          E.N = it.N;
+          E.kp = tmk::small_kp(it.k);
+          E.Np = tmk::small_np(it.N);
+          E.flags = it.tall ? tmk::kTall : 0u;
+          E.tile_start = uint32_t(start);
+          E.tiles_per = 1u;
+          E.count = it.count;
+          ++i;
+          // a run of single matrices of this shape: one pointer-table entry
+          auto same = [&](size_t j) {
+            const Item& v = items[idx[j]];
+            return it.count == 1u && v.count == 1u && v.k == it.k && v.N == it.N && v.tall == it.tall;
+          };
+          if (i < idx.size() && same(i) && xp + 2 <= tmk::kMaxSmallPtrs) {
+            E.flags |= tmk::kPtrTab;
+            E.xbase = uint32_t(xp);
+            P.xp[xp++] = it.x;
+            while (i < idx.size() && same(i) && xp < tmk::kMaxSmallPtrs) P.xp[xp++] = items[idx[i++]].x;
+            E.count = uint32_t(xp) - E.xbase;
+          }
+          start += E.count;
+          ++P.nent;
+          if (start >= (uint64_t(1) << 31))
+            return fail(TM_ERR_UNSUPPORTED, "too many matrices in one launch");
+        }
+        P.total = int32_t(start);
+        TimedLaunch tl{int(tmk::kKindSmall), nullptr, nullptr};
+        if (g_timing && pl.timed) {
+          if (hipEventCreate(&tl.start) != hipSuccess || hipEventCreate(&tl.stop) != hipSuccess)
+            return fail(TM_ERR_HIP, "hipEventCreate failed");
+          (void)hipEventRecord(tl.start, pl.st);
+        }
+        const hipError_t e = tmk::launch_small_bf16(F, big, P, pl.st);
+        if (tl.start) {
+          (void)hipEventRecord(tl.stop, pl.st);
+          g_timed.push_back(tl);
+        }
+        if (e != hipSuccess) return fail(TM_ERR_HIP, std::string("kernel launch: ") + hipGetErrorString(e));
+      }
+    }
+  return TM_OK;
+}
+
 // Scale vector s from the first Gram (its flags carry the row partials):
 // AOL (Algorithm 2, second line) s_i = 1 / sqrt(row sum of |A0|); Schatten-4
 // the uniform ||A0||_F^(-1/2), summed from the squares' row partials.  `part`
@@ -559,6 +645,19 @@ tm_status run_locked(std::vector<Item>& items, int esz, int iters, const float* 
                      int precond, hipStream_t st, int dev, char* ext_ws = nullptr,
                      uint64_t ext_bytes = 0) {
   tm_status s = TM_OK;
+  // bf16 calls made only of small matrices: the fused kernel, one launch
+  // (TM_DISABLE_FUSED in the environment keeps them on the tiled kernels)
+  if (esz == 2 && iters >= 1 && std::all_of(items.begin(), items.end(), small_eligible) &&
+      std::getenv("TM_DISABLE_FUSED") == nullptr) {
+    Plan pl;
+    pl.items = &items;
+    pl.esz = esz;
+    pl.st = st;
+    pl.ws = nullptr;
+    pl.timed = ext_ws == nullptr;
+    (void)dev;
+    return plan_small(pl, iters, coeffs, precond);
+  }
   // A call of more than kMaxEntries items runs every phase as several
   // launches; largest products first, so the last, partly filled launch
   // holds the shortest tiles.  Each matrix's arithmetic does not depend on

@@ -93,6 +93,36 @@ struct Phase {
 };
 static_assert(sizeof(Entry) == 48 && sizeof(Phase) <= 3200, "kernel arguments of one launch");
 
+// Fused small-matrix path (bf16, every matrix of the call with k <= 128 and
+// its zero-padded Y, A and B within the LDS): one workgroup per matrix runs
+// every iteration in one launch.  Entries as in Phase (tiles_per = 1); the
+// per-iteration coefficients travel with the launch.
+constexpr int kMaxSmallEntries = 32;
+constexpr int kMaxSmallPtrs = 64;
+constexpr int kMaxIters = 64;           // TM_MAX_ITERS
+constexpr int kSmallMaxK = 128;
+
+struct SmallPhase {
+  Entry e[kMaxSmallEntries];
+  char* xp[kMaxSmallPtrs];
+  float coef[kMaxIters][3];
+  int32_t nent;
+  int32_t total;       // workgroups (matrices) in the launch
+  int32_t iters;
+  int32_t precond;     // TM_PRECOND_*
+};
+static_assert(sizeof(SmallPhase) <= 3200, "kernel arguments of one launch");
+
+// LDS bytes of the fused path for one matrix: Y (kp x Np), A and B (kp x kp),
+// bf16 rows padded by 16 bytes, plus the row-sum scratch (kp / 16 x kp fp32),
+// the scale vector and the reduction scratch (32 x 4 fp32).
+TM_HD uint32_t small_kp(uint32_t k) { return (k + 31u) / 32u * 32u; }
+TM_HD uint32_t small_np(uint32_t N) { return (N + 31u) / 32u * 32u; }
+TM_HD uint64_t small_lds_bytes(uint32_t k, uint32_t N) {
+  const uint64_t kp = small_kp(k), Np = small_np(N);
+  return kp * (2 * Np + 16) + 2 * kp * (2 * kp + 16) + (kp / 16) * kp * 4 + kp * 4 + 512;
+}
+
 // Optimizer step (fp32 parameters): elementwise launches over the elements of
 // up to kMaxOptEntries matrices, blocks of kOptBlock elements.
 constexpr int kMaxOptEntries = 32;
@@ -130,7 +160,7 @@ TM_HD int cfg_tile(int cfg) { return cfg == 0 ? 256 : (cfg == 1 ? 128 : (cfg == 
 // The numbering matches the TM_PHASE_* timing phases of turbomuon.h.
 enum Kind { kKindTransposeIn, kKindFrob, kKindGram, kKindAolVector, kKindPoly,
             kKindUpdate, kKindApplyScale, kKindCopyOut, kKindLoadIn, kKindScaleA,
-            kKindOptMomentum, kKindOptApply, kNumKinds };
+            kKindOptMomentum, kKindOptApply, kKindSmall, kNumKinds };
 constexpr int kTransposeTile = 64;
 constexpr int kElemBlock = 2048;     // elements per block of the elementwise kernels
 

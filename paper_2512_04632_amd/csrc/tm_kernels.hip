@@ -608,7 +608,9 @@ __global__ __launch_bounds__(256) void k_frob_partial(const Phase P) {
   const Loc L = locate(P, blockIdx.x);
   const Entry& E = P.e[L.ent];
   const bool from_part = (P.flags & kFromPart) != 0u;
-  const int64_t nb = int64_t(cdiv(E.kp, uint32_t(max(P.aux, 1))));
+  // partials past column k are zero: their count follows k, not the padding,
+  // so the chunks (and the sum) do not depend on the tile size
+  const int64_t nb = int64_t(cdiv(E.k, uint32_t(max(P.aux, 1))));
   const int64_t total = from_part ? nb * E.k : int64_t(E.k) * E.N;
   const int64_t chunk = (total + kFrobBlocks - 1) / kFrobBlocks;
   const int64_t lo = chunk * L.tile, hi = min(total, lo + chunk);

@@ -146,6 +146,8 @@ WORKLOADS = {
     "resnet_conv_64": {"dtype": "bf16", "entries":
                        [(16, 64, 576, 1.0), (16, 128, 1152, 1.0),
                         (16, 256, 2304, 1.0), (16, 512, 4608, 1.0)]},
+    # its first stage alone: 16 matrices of 64 x 576 (the fused small-matrix kernel)
+    "resnet_conv_64x576_b16": {"dtype": "bf16", "entries": [(16, 64, 576, 1.0)]},
 }
 
 
