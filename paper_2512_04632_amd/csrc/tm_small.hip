@@ -36,7 +36,7 @@ typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
 typedef short s16x4_t __attribute__((ext_vector_type(4)));
 
-constexpr int NT = 256;                      // 4 waves in a 2 x 2 grid
+constexpr int NR = 256;   // threads of the reduction and product structure: 4 waves in a 2 x 2 grid
 constexpr float kTiny = 1.17549435e-38f;     // FLT_MIN: smaller sums give a zero scale
 
 __device__ inline float bf2f(uint16_t v) { return __uint_as_float(uint32_t(v) << 16); }
@@ -117,6 +117,7 @@ __device__ inline uint16_t half_of(const uint4& v, int t) {
 // the matrix reads X's first element instead and its value is replaced by
 // zero, so that no load sits behind a branch (which would make each wait for
 // the previous one).
+template <int NT>
 __device__ inline void load_y(const Geo& G, const uint16_t* X, bool tall) {
   const int tid = threadIdx.x;
   const bool vec = (reinterpret_cast<uintptr_t>(X) & 15u) == 0u;
@@ -215,6 +216,7 @@ __device__ inline void load_y(const Geo& G, const uint16_t* X, bool tall) {
 
 // X = Y (wide) or Y^T (tall), the unpadded part; LB pieces read from LDS per
 // thread before they are stored.
+template <int NT>
 __device__ inline void store_y(const Geo& G, uint16_t* X, bool tall) {
   const int tid = threadIdx.x;
   const bool vec = (reinterpret_cast<uintptr_t>(X) & 15u) == 0u;
@@ -395,7 +397,7 @@ __device__ inline float part64(const Geo& G, int b, int i) {
 // xor butterfly over offsets 32, 16, ..., 1 and the four wave sums added in
 // order; the chunk sums are then added in order.  Every thread forms its sums
 // of CG chunks (LB terms read before they are added), then their CG
-// butterflies run side by side.
+// butterflies run side by side.  Only the first 256 threads take part.
 template <bool SQ, class V>
 __device__ inline float chunked_sum(const Geo& G, uint32_t total, V term) {
   constexpr int CG = 8;                          // chunks reduced side by side
@@ -405,13 +407,13 @@ __device__ inline float chunked_sum(const Geo& G, uint32_t total, V term) {
     float x[CG];
 #pragma unroll
     for (int j = 0; j < CG; ++j) {
-      const uint32_t lo = chunk * uint32_t(c0 + j), hi = min(total, lo + chunk);
+      const uint32_t lo = chunk * uint32_t(c0 + j), hi = threadIdx.x < NR ? min(total, lo + chunk) : 0u;
       x[j] = 0.f;
-      for (uint32_t q = lo + threadIdx.x; q < hi; q += LB * NT) {
+      for (uint32_t q = lo + threadIdx.x; q < hi; q += LB * NR) {
         float e[LB];
 #pragma unroll
         for (int u = 0; u < LB; ++u) {
-          const uint32_t qq = q + uint32_t(u * NT);
+          const uint32_t qq = q + uint32_t(u * NR);
           e[u] = term(qq < hi ? qq : lo);
           e[u] = qq < hi ? e[u] : 0.f;
         }
@@ -426,7 +428,7 @@ __device__ inline float chunked_sum(const Geo& G, uint32_t total, V term) {
     for (int off = 32; off >= 1; off >>= 1)
 #pragma unroll
       for (int j = 0; j < CG; ++j) x[j] += __shfl_xor(x[j], off, 64);
-    if (lane == 0) {
+    if (lane == 0 && w < 4) {
 #pragma unroll
       for (int j = 0; j < CG; ++j) G.red[4 * (c0 + j) + w] = x[j];
     }
@@ -438,9 +440,14 @@ __device__ inline float chunked_sum(const Geo& G, uint32_t total, V term) {
   return r;
 }
 
-// One matrix per workgroup, every iteration in LDS.  F = kp / 32.
-template <int F, int LDSB>
-__global__ __launch_bounds__(NT) void k_small_ns(const SmallPhase P) {
+// One matrix per workgroup, every iteration in LDS.  F = kp / 32; NW waves:
+// the first four form the 2 x 2 grid of the Gram and polynomial products and
+// the reductions, all NW share the loads, the stores and the update (8 for
+// F <= 2: two waves per SIMD hide each other's LDS and matrix-core
+// latencies; the register footprint of F = 3, 4 allows one).
+template <int F, int LDSB, int NW>
+__global__ __launch_bounds__(64 * NW) void k_small_ns(const SmallPhase P) {
+  constexpr int NT = 64 * NW;
   __shared__ __attribute__((aligned(16))) char smem[LDSB];
   int mat;
   const Entry& E = P.e[locate(P, int(blockIdx.x), mat)];
@@ -449,10 +456,12 @@ __global__ __launch_bounds__(NT) void k_small_ns(const SmallPhase P) {
   const Geo G = geometry(smem, int(E.k), int(E.N));
   const int precond = P.precond;
   const bool scaled = precond != TM_PRECOND_NONE;
+  const bool from_gram = precond == TM_PRECOND_AOL || precond == TM_PRECOND_SCHATTEN4;
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int lr = lane & 15, g = lane >> 4;
+  const bool prod = w < 4;   // a wave of the product grid
 
-  load_y(G, X, tall);
+  load_y<NT>(G, X, tall);
   __syncthreads();
 
   // Frobenius scale (Algorithm 1), over the elements of X in its storage order
@@ -473,10 +482,12 @@ __global__ __launch_bounds__(NT) void k_small_ns(const SmallPhase P) {
     const float ca = P.coef[it][0], cb = P.coef[it][1], cc = P.coef[it][2];
     const bool first = it == 0;
     // ---- Gram A = Y Y^T (fp32 accumulators)
-    sym_product<F>(acc, G.y, G.ry, G.Np);
+    if (prod) {
+      sym_product<F>(acc, G.y, G.ry, G.Np);
+      if (first && from_gram) row_sums16<F>(G, acc, precond == TM_PRECOND_SCHATTEN4);
+    }
     if (first && scaled) {
-      if (precond == TM_PRECOND_AOL || precond == TM_PRECOND_SCHATTEN4) {
-        row_sums16<F>(G, acc, precond == TM_PRECOND_SCHATTEN4);
+      if (from_gram) {
         __syncthreads();
         const int nb = (G.k + 63) / 64;   // 64-column partials per row
         if (precond == TM_PRECOND_AOL) {
@@ -502,43 +513,47 @@ __global__ __launch_bounds__(NT) void k_small_ns(const SmallPhase P) {
     }
     // A (bf16), written through its transpose: 4 consecutive rows of one
     // column of the lane's block become 4 consecutive elements of a row
+    if (prod) {
 #pragma unroll
-    for (int fm = 0; fm < F; ++fm)
+      for (int fm = 0; fm < F; ++fm)
 #pragma unroll
-      for (int fn = 0; fn < F; ++fn) {
-        const int i0 = row0<F>(fm), j = col0<F>(fn);
-        uint16_t o[4];
+        for (int fn = 0; fn < F; ++fn) {
+          const int i0 = row0<F>(fm), j = col0<F>(fn);
+          uint16_t o[4];
 #pragma unroll
-        for (int u = 0; u < 4; ++u) {
-          const float x = acc[fm][fn][u];
-          o[u] = f2bf(first && scaled ? x * (G.s[i0 + u] * G.s[j]) : x);
+          for (int u = 0; u < 4; ++u) {
+            const float x = acc[fm][fn][u];
+            o[u] = f2bf(first && scaled ? x * (G.s[i0 + u] * G.s[j]) : x);
+          }
+          *reinterpret_cast<uint2*>(G.a + j * G.ra + i0 * 2) = *reinterpret_cast<const uint2*>(o);
         }
-        *reinterpret_cast<uint2*>(G.a + j * G.ra + i0 * 2) = *reinterpret_cast<const uint2*>(o);
-      }
+    }
     __syncthreads();
     // ---- polynomial B~ = b A + c A A + a I (C = B~ diag(s) after a scaling)
-    sym_product<F>(acc, G.a, G.ra, G.kp);
+    if (prod) {
+      sym_product<F>(acc, G.a, G.ra, G.kp);
 #pragma unroll
-    for (int fm = 0; fm < F; ++fm)
+      for (int fm = 0; fm < F; ++fm)
 #pragma unroll
-      for (int fn = 0; fn < F; ++fn) {
-        const int i0 = row0<F>(fm), j = col0<F>(fn);
-        const uint2 araw = *reinterpret_cast<const uint2*>(G.a + j * G.ra + i0 * 2);
-        const uint16_t* av = reinterpret_cast<const uint16_t*>(&araw);
-        uint16_t o[4];
+        for (int fn = 0; fn < F; ++fn) {
+          const int i0 = row0<F>(fm), j = col0<F>(fn);
+          const uint2 araw = *reinterpret_cast<const uint2*>(G.a + j * G.ra + i0 * 2);
+          const uint16_t* av = reinterpret_cast<const uint16_t*>(&araw);
+          uint16_t o[4];
 #pragma unroll
-        for (int u = 0; u < 4; ++u) {
-          const float x = cb * bf2f(av[u]) + cc * acc[fm][fn][u] + (i0 + u == j ? ca : 0.f);
-          // stored at (j, i0 + u): B~ is symmetric; C[j][i] = B~_ij s_i
-          o[u] = f2bf(first && scaled ? x * G.s[i0 + u] : x);
+          for (int u = 0; u < 4; ++u) {
+            const float x = cb * bf2f(av[u]) + cc * acc[fm][fn][u] + (i0 + u == j ? ca : 0.f);
+            // stored at (j, i0 + u): B~ is symmetric; C[j][i] = B~_ij s_i
+            o[u] = f2bf(first && scaled ? x * G.s[i0 + u] : x);
+          }
+          *reinterpret_cast<uint2*>(G.b + j * G.ra + i0 * 2) = *reinterpret_cast<const uint2*>(o);
         }
-        *reinterpret_cast<uint2*>(G.b + j * G.ra + i0 * 2) = *reinterpret_cast<const uint2*>(o);
-      }
+    }
     __syncthreads();
     // ---- update Y' = B~ Y (C X0 at the first iteration), in place.  Every
     // wave holds all of B~'s fragments in registers; wave w owns the
-    // 16-column blocks w, w + 4, ... of Y, reads all their rows (the next
-    // block's while the current one multiplies) and writes them back.
+    // 16-column blocks w, w + NW, ... of Y, reads all their rows and writes
+    // them back.
     {
       constexpr int FR = 2 * F;                   // 16-row blocks of kp
       uint4 bq[F][FR];                            // [K slice][row block]
@@ -582,32 +597,43 @@ __global__ __launch_bounds__(NT) void k_small_ns(const SmallPhase P) {
               *reinterpret_cast<const uint2*>(o);
         }
       };
-      // Two blocks (c, c + 4) per step: the fragments of the step's second
-      // block and of the next step's first are read ahead, and the first
-      // block's results are converted and stored while the second one's
-      // products run.  Reads past the last block land in the row padding or
-      // the next LDS region and are discarded.
+      // The fragments of the wave's next block are read while the current
+      // one multiplies; with one wave per SIMD, two blocks (c, c + NW) per
+      // step, the first one's results converted and stored while the second
+      // one's products run.  Reads past the last block land in the row
+      // padding or the next LDS region and are discarded.
       uint4 ya[F], yb[F];
       f32x4_t ua[FR], ub[FR];
       yfrag(ya, w);
-      for (int c = w; c < nblk; c += 8) {
-        yfrag(yb, c + 4);
-        mult(ua, ya);
-        yfrag(ya, c + 8);
-        mult(ub, yb);
-        put(ua, c);
-        if (c + 4 < nblk) put(ub, c + 4);
+      if constexpr (NW == 8) {
+        for (int c = w; c < nblk; c += NW) {
+          yfrag(yb, c + NW);
+          mult(ua, ya);
+          put(ua, c);
+#pragma unroll
+          for (int s = 0; s < F; ++s) ya[s] = yb[s];
+        }
+      } else {
+        for (int c = w; c < nblk; c += 2 * NW) {
+          yfrag(yb, c + NW);
+          mult(ua, ya);
+          yfrag(ya, c + 2 * NW);
+          mult(ub, yb);
+          put(ua, c);
+          if (c + NW < nblk) put(ub, c + NW);
+        }
       }
     }
     __syncthreads();
   }
-  store_y(G, X, tall);
+  store_y<NT>(G, X, tall);
 }
 
 template <int F>
 static hipError_t launch_f(int big, const SmallPhase& P, hipStream_t st) {
-  if (big) hipLaunchKernelGGL((k_small_ns<F, 160 * 1024>), dim3(P.total), dim3(NT), 0, st, P);
-  else hipLaunchKernelGGL((k_small_ns<F, 64 * 1024>), dim3(P.total), dim3(NT), 0, st, P);
+  constexpr int NW = F <= 2 ? 8 : 4;
+  if (big) hipLaunchKernelGGL((k_small_ns<F, 160 * 1024, NW>), dim3(P.total), dim3(64 * NW), 0, st, P);
+  else hipLaunchKernelGGL((k_small_ns<F, 64 * 1024, NW>), dim3(P.total), dim3(64 * NW), 0, st, P);
   return hipGetLastError();
 }
 
