@@ -29,6 +29,10 @@ def _inputs(case):
         return [rn(2, 700, 300).bfloat16()]
     if case == "batched_f32":
         return [rn(2, 192, 320)]
+    if case == "fused_bf16":        # k <= 128: the single-launch small-matrix kernel
+        return [rn(16, 64, 576).bfloat16()]
+    if case == "fused_grouped_bf16":
+        return [rn(m, n).bfloat16() for m, n in [(64, 576), (576, 64), (17, 33), (128, 320)]]
     return [rn(m, n).bfloat16() for m, n in [(64, 576), (300, 200), (128, 1152), (768, 768)]]
 
 
@@ -44,7 +48,8 @@ def _busy_work():
     return float((a @ a).sum().item())
 
 
-@pytest.mark.parametrize("case", ["batched_bf16", "tall_bf16", "batched_f32", "grouped_bf16"])
+@pytest.mark.parametrize("case", ["batched_bf16", "tall_bf16", "batched_f32", "grouped_bf16",
+                                  "fused_bf16", "fused_grouped_bf16"])
 def test_replays_match_eager(case):
     log(f"case: graph capture and replay, {case}")
     X0 = _inputs(case)

@@ -13,6 +13,8 @@ from paper_2512_04632_amd import _lib as tm  # noqa: E402
 from paper_2512_04632_amd.optim import TurboMuon  # noqa: E402
 
 SHAPES = [(64, 96), (96, 64), (128, 128), (17, 300), (300, 17), (1, 5), (768, 3072), (3072, 768)]
+# only matrices the fused small-matrix kernel takes (k <= 128, within one compute unit's LDS)
+SMALL_SHAPES = [(64, 96), (96, 64), (128, 128), (17, 300), (300, 17), (1, 5), (64, 576)]
 
 
 def f32(x):
@@ -27,20 +29,21 @@ def host(t):
     return t.detach().cpu().numpy().astype(np.float64)
 
 
+@pytest.mark.parametrize("shapes", [SHAPES, SMALL_SHAPES], ids=["mixed", "small"])
 @pytest.mark.parametrize("nesterov", [True, False])
 @pytest.mark.parametrize("wd", [0.0, 0.05])
-def test_two_grouped_steps_match_the_oracle(nesterov, wd):
-    log(f"case: grouped optimizer steps nesterov={nesterov} wd={wd} shapes={SHAPES}")
+def test_two_grouped_steps_match_the_oracle(nesterov, wd, shapes):
+    log(f"case: grouped optimizer steps nesterov={nesterov} wd={wd} shapes={shapes}")
     lr, mu = 0.02, 0.9
-    Ws = [f32(0.02 * synth.gaussian_matrix(m, n, 10 + i)) for i, (m, n) in enumerate(SHAPES)]
-    Ms = [f32(0.1 * synth.gaussian_matrix(m, n, 20 + i)) for i, (m, n) in enumerate(SHAPES)]
+    Ws = [f32(0.02 * synth.gaussian_matrix(m, n, 10 + i)) for i, (m, n) in enumerate(shapes)]
+    Ms = [f32(0.1 * synth.gaussian_matrix(m, n, 20 + i)) for i, (m, n) in enumerate(shapes)]
     tW, tM = [dev(w) for w in Ws], [dev(m) for m in Ms]
     for step in range(2):
-        Gs = [f32(synth.power_law_matrix(m, n, 0.8, 100 * step + i)) for i, (m, n) in enumerate(SHAPES)]
+        Gs = [f32(synth.power_law_matrix(m, n, 0.8, 100 * step + i)) for i, (m, n) in enumerate(shapes)]
         tG = [dev(g) for g in Gs]
         tm.muon_step_grouped(tW, tG, tM, lr, mu, nesterov, wd)
         torch.cuda.synchronize()
-        for i, (m, n) in enumerate(SHAPES):
+        for i, (m, n) in enumerate(shapes):
             Wr, Mr, Or = O.muon_step(Ws[i], Gs[i], Ms[i], lr, mu, nesterov, wd)
             Wg, Mg = host(tW[i]), host(tM[i])
             # momentum: one fp32 multiply-add per element
