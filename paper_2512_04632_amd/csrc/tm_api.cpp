@@ -64,6 +64,7 @@ struct TimedLaunch {
 bool g_timing = false;
 std::vector<TimedLaunch> g_timed;
 static_assert(int(tmk::kNumKinds) == TM_NUM_PHASES, "one timing phase per kernel kind");
+static_assert(tmk::kMaxIters == TM_MAX_ITERS, "the fused kernel's descriptor holds every iteration");
 double g_time_ms[TM_NUM_PHASES];
 int64_t g_time_n[TM_NUM_PHASES];
 
