@@ -398,13 +398,44 @@ tm_status launch(const Plan& pl, int kind, int cfg, int src, int dst, float a, f
     P.aux = aux;
     P.tail_base = 0;
     tm_status s = TM_OK;
+    // A bf16 matrix-core launch of more than one wave whose entries' tiles
+    // differ in K deals whole matrices round-robin to the XCDs (kByMatrix):
+    // the default chunks of 32 consecutive tiles per XCD would give the first
+    // XCDs all the long tiles of a largest-first launch.
+    const bool mc0 = kind == tmk::kKindGram || kind == tmk::kKindPoly || kind == tmk::kKindUpdate;
+    bool by_matrix = false;
+    if (pl.esz == 2 && mc0 && P.total > kWave) {
+      uint32_t kmin = UINT32_MAX, kmax = 0;
+      for (int e = 0; e < P.nent; ++e) {
+        if (P.e[e].tiles_per == 0u) continue;
+        const uint32_t K = kind == tmk::kKindGram ? P.e[e].Np : P.e[e].kp;
+        kmin = std::min(kmin, K);
+        kmax = std::max(kmax, K);
+      }
+      if (kmin != kmax) {
+        uint64_t q[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+        uint64_t g0 = 0;
+        for (int e = 0; e < P.nent; ++e) {
+          const uint64_t c = P.e[e].count;
+          for (int x = 0; x < 8; ++x) {
+            const uint64_t i0 = uint64_t((x - int(g0 & 7u) + 8) & 7);
+            q[x] += (i0 < c ? (c - 1 - i0) / 8 + 1 : 0) * P.e[e].tiles_per;
+          }
+          g0 += c;
+        }
+        const uint64_t qmax = *std::max_element(q, q + 8);
+        P.flags |= tmk::kByMatrix;
+        P.total = int32_t(8 * qmax);
+        by_matrix = true;
+      }
+    }
     // bf16 matrix-core phases on 256 x 256 tiles whose last wave would be at
     // most a quarter full: the full waves run as usual, the remaining tiles as
     // 2 x 2 sub-tiles of 128 x 128 in a second launch that fits in one wave
     // (same per-element arithmetic, four times the blocks for the idle units);
     // an update tail of at most 16 tiles as 4 x 4 sub-tiles of 64 x 64.
     const bool mc = kind == tmk::kKindGram || kind == tmk::kKindPoly || kind == tmk::kKindUpdate;
-    const int tail = (pl.esz == 2 && ccfg == 0 && mc && P.total > kWave && P.total % kWave <= kWave / 4)
+    const int tail = (!by_matrix && pl.esz == 2 && ccfg == 0 && mc && P.total > kWave && P.total % kWave <= kWave / 4)
                          ? P.total % kWave
                          : 0;
     if (tail > 0) {

@@ -713,6 +713,30 @@ __device__ inline Loc locate(const Phase& P, int lid) {
   return L;
 }
 
+// kByMatrix: workgroup p runs on XCD p % 8 (round-robin dispatch), and XCD x's
+// workgroups take, in launch order, the tiles of the launch's matrices whose
+// index is x mod 8: each XCD gets an eighth of every kind of matrix (balanced
+// when tile costs differ between entries) and a matrix's tiles share one L2.
+// False for the workgroups past the end of their XCD's list.
+__device__ inline bool locate_by_matrix(const Phase& P, int p, Loc& L) {
+  const int x = p & 7;
+  int j = p >> 3, g0 = 0;
+  for (int e = 0; e < P.nent; ++e) {
+    const int c = int(P.e[e].count), tp = int(P.e[e].tiles_per);
+    const int i0 = (x - (g0 & 7) + 8) & 7;        // first matrix of the entry on XCD x
+    const int nt = (i0 < c ? (c - 1 - i0) / 8 + 1 : 0) * tp;
+    if (j < nt) {
+      L.ent = e;
+      L.mat = i0 + 8 * (j / tp);
+      L.tile = j - (j / tp) * tp;
+      return true;
+    }
+    j -= nt;
+    g0 += c;
+  }
+  return false;
+}
+
 __device__ inline char* ws_of(const Phase& P, const Entry& E, int mat) {
   return P.ws + (uint64_t(E.ws256) << 8) + uint64_t(mat) * ws_layout(E.kp, E.Np, 2).total;
 }
@@ -759,7 +783,11 @@ __device__ inline bool sym_tile(const Phase& P, Loc& L, int& I, int& J) {
     J = 2 * J2 + (sub & 1);
     return true;
   }
-  L = locate(P, xcd_remap(blockIdx.x, P.total));
+  if (P.flags & kByMatrix) {
+    if (!locate_by_matrix(P, int(blockIdx.x), L)) return false;
+  } else {
+    L = locate(P, xcd_remap(blockIdx.x, P.total));
+  }
   tri_tile(L.tile, int(P.e[L.ent].kp) / T, I, J);
   return true;
 }
@@ -1116,8 +1144,10 @@ __global__ __launch_bounds__(Tile<T>::NT) void k_update_fast(const Phase P) {
   const bool tail = (P.flags & kTail) != 0u;
   const int F = !tail ? 1 : ((P.flags & kTail4) ? 4 : 2);
   const int FF = F * F;
-  const Loc L = tail ? locate(P, P.tail_base + int(blockIdx.x) / FF)
-                     : locate(P, xcd_remap(blockIdx.x, P.total));
+  Loc L;
+  if (tail) L = locate(P, P.tail_base + int(blockIdx.x) / FF);
+  else if (!(P.flags & kByMatrix)) L = locate(P, xcd_remap(blockIdx.x, P.total));
+  else if (!locate_by_matrix(P, int(blockIdx.x), L)) return;
   const Entry& E = P.e[L.ent];
   const int kp = int(E.kp), Np = int(E.Np), k = int(E.k), N = int(E.N);
   const int TL = F * T;

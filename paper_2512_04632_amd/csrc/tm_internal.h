@@ -54,6 +54,8 @@ constexpr uint32_t kFromPart = 64u;  // Frobenius-partial kernel sums the Gram's
 constexpr uint32_t kTail = 128u;  // matrix-core kernels: blocks are 2 x 2 sub-tiles of the
                                   // tiles of twice their size from tail_base on
 constexpr uint32_t kTail4 = 512u; // with kTail (update only): 4 x 4 sub-tiles of a quarter size
+constexpr uint32_t kByMatrix = 1024u; // matrix-core kernels: XCD x runs every tile of the launch's
+                                      // matrices x, x + 8, ... (blocks p with p % 8 == x)
 constexpr uint32_t kFuseS = 256u; // bf16 rescale of A0: the AOL vector is summed in the same
                                   // kernel from the Gram's row partials (aux columns each)
 
