@@ -398,13 +398,15 @@ tm_status launch(const Plan& pl, int kind, int cfg, int src, int dst, float a, f
     P.aux = aux;
     P.tail_base = 0;
     tm_status s = TM_OK;
-    // A bf16 matrix-core launch of more than one wave whose entries' tiles
-    // differ in K deals whole matrices round-robin to the XCDs (kByMatrix):
-    // the default chunks of 32 consecutive tiles per XCD would give the first
-    // XCDs all the long tiles of a largest-first launch.
+    // A bf16 matrix-core launch whose entries' tiles differ in K deals whole
+    // matrices round-robin to the XCDs (kByMatrix) when that splits the work
+    // evenly (every XCD within 10% of an eighth, the cost of a tile taken as
+    // its K): the default chunks of consecutive tiles per XCD would give the
+    // first XCDs all the long tiles of a largest-first launch.  A launch of a
+    // few matrices keeps the chunks.
     const bool mc0 = kind == tmk::kKindGram || kind == tmk::kKindPoly || kind == tmk::kKindUpdate;
     bool by_matrix = false;
-    if (pl.esz == 2 && mc0 && P.total > kWave) {
+    if (pl.esz == 2 && mc0) {
       uint32_t kmin = UINT32_MAX, kmax = 0;
       for (int e = 0; e < P.nent; ++e) {
         if (P.e[e].tiles_per == 0u) continue;
@@ -414,19 +416,29 @@ tm_status launch(const Plan& pl, int kind, int cfg, int src, int dst, float a, f
       }
       if (kmin != kmax) {
         uint64_t q[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+        double cost[8] = {0, 0, 0, 0, 0, 0, 0, 0};
         uint64_t g0 = 0;
         for (int e = 0; e < P.nent; ++e) {
           const uint64_t c = P.e[e].count;
+          const double K = kind == tmk::kKindGram ? P.e[e].Np : P.e[e].kp;
           for (int x = 0; x < 8; ++x) {
             const uint64_t i0 = uint64_t((x - int(g0 & 7u) + 8) & 7);
-            q[x] += (i0 < c ? (c - 1 - i0) / 8 + 1 : 0) * P.e[e].tiles_per;
+            const uint64_t t = (i0 < c ? (c - 1 - i0) / 8 + 1 : 0) * P.e[e].tiles_per;
+            q[x] += t;
+            cost[x] += double(t) * K;
           }
           g0 += c;
         }
-        const uint64_t qmax = *std::max_element(q, q + 8);
-        P.flags |= tmk::kByMatrix;
-        P.total = int32_t(8 * qmax);
-        by_matrix = true;
+        double sum = 0.0, top = 0.0;
+        for (int x = 0; x < 8; ++x) {
+          sum += cost[x];
+          top = std::max(top, cost[x]);
+        }
+        if (top <= 1.1 * sum / 8.0) {
+          P.flags |= tmk::kByMatrix;
+          P.total = int32_t(8 * *std::max_element(q, q + 8));
+          by_matrix = true;
+        }
       }
     }
     // bf16 matrix-core phases on 256 x 256 tiles whose last wave would be at

@@ -300,13 +300,13 @@ def test_grouped_gpt2_small_matches_single_calls_bitwise():
 
 
 def test_grouped_mixed_k_dealt_by_matrix_matches_single_calls():
-    """A grouped launch of more than one wave whose Gram tiles differ in K deals
-    whole matrices round-robin to the XCDs: 20 matrices of 256 x 2048 and 30 of
-    256 x 512 (500 Gram tiles of 64, queues of unequal length per XCD, so some
-    workgroups find no tile).  Every matrix equals its own single call bit for bit,
-    and a sample of each shape the oracle."""
-    log("case: grouped 20 x 256x2048 + 30 x 256x512, by-matrix dealing")
-    shapes = [(256, 2048)] * 20 + [(256, 512)] * 30
+    """A grouped launch whose Gram tiles differ in K, and whose matrices split
+    evenly over the 8 XCDs, deals whole matrices round-robin to the XCDs: 24
+    matrices of 256 x 2048 and 30 of 256 x 512 (540 Gram tiles of 64; queues of 70
+    and 60 tiles per XCD, so some workgroups find no tile).  Every matrix equals
+    its own single call bit for bit, and a sample of each shape the oracle."""
+    log("case: grouped 24 x 256x2048 + 30 x 256x512, by-matrix dealing")
+    shapes = [(256, 2048)] * 24 + [(256, 512)] * 30
     Xs = [make_input(m, n, 0.8, 500 + i, "bf16") for i, (m, n) in enumerate(shapes)]
     ts = [to_device(X, "bf16") for X in Xs]
     tm.orthogonalize_grouped(ts, 4, None, "aol")
@@ -315,7 +315,7 @@ def test_grouped_mixed_k_dealt_by_matrix_matches_single_calls():
         single = to_device(Xs[i], "bf16")
         tm.orthogonalize(single, 4, None, "aol")
         assert torch.equal(ts[i], single), i
-    for i in (0, 19, 20, 49):
+    for i in (0, 23, 24, 53):
         e = relF(from_device(ts[i]), O.orthogonalize(Xs[i], 4, None, "aol"))
         log(f"matrix {i}: relF={e:.3e}")
         assert e <= BF16_TOL
