@@ -202,3 +202,64 @@ def test_noalloc_small_call_is_fused():
     tm.orthogonalize_noalloc(a, 4, None, "aol")
     torch.cuda.synchronize()
     assert torch.equal(a.view(torch.int16), b.view(torch.int16))
+
+
+def test_fused_every_iteration_row_of_the_descriptor():
+    """TM_MAX_ITERS iterations: every coefficient row the launch descriptor holds is
+    used (a normalised quintic schedule cycled to 64 rows), bitwise equal to the
+    tiled kernels."""
+    rows = [SCHEDULE5[i % 5] for i in range(tm.TM_MAX_ITERS)]
+    Xs = [make_input(40, 200, 1.0, 77 + b, "bf16") for b in range(2)]
+    f = run_batched(Xs, tm.TM_MAX_ITERS, "aol", rows)
+    with tiled_only():
+        g = run_batched(Xs, tm.TM_MAX_ITERS, "aol", rows)
+    assert torch.equal(f.view(torch.int16), g.view(torch.int16))
+    e = relF(from_device(f[0]), O.orthogonalize(Xs[0], tm.TM_MAX_ITERS, rows, "aol"))
+    log(f"t=64 relF={e:.3e}")
+    assert e <= BF16_TOL
+
+
+@pytest.mark.parametrize("seed", range(4))
+def test_fused_random_shapes_equal_tiled(seed):
+    """Seeded random shapes across the fused kernel's range (k <= 128, both LDS
+    variants, both orientations) and pre-conditionings: bitwise the tiled kernels."""
+    rng = np.random.default_rng(900 + seed)
+    shapes = []
+    while len(shapes) < 6:
+        k = int(rng.integers(1, 129))
+        N = int(rng.integers(k, 1200))
+        m, n = (k, N) if rng.integers(2) else (N, k)
+        kp, Np = -(-k // 32) * 32, -(-N // 32) * 32
+        lds = kp * (2 * Np + 16) + 2 * kp * (2 * kp + 16) + (kp // 16) * kp * 4 + kp * 4 + 512
+        if lds <= 160 * 1024:
+            shapes.append((m, n))
+    precond = ("aol", "frobenius", "schatten4", "aol")[seed]
+    iters = (4, 5, 4, 2)[seed]
+    log(f"case: random fused shapes {shapes} {precond} t={iters}")
+    Xs = [make_input(m, n, 0.9, 1000 * seed + i, "bf16") for i, (m, n) in enumerate(shapes)]
+    counts = launches(lambda: run_grouped(Xs, iters, precond))
+    # one launch per (kp / 32, LDS variant) class present in the group
+    assert counts["fused"] >= 1 and all(v == 0 for p, v in counts.items() if p != "fused"), counts
+    f = run_grouped(Xs, iters, precond)
+    with tiled_only():
+        g = run_grouped(Xs, iters, precond)
+    for i in range(len(shapes)):
+        assert torch.equal(f[i].view(torch.int16), g[i].view(torch.int16)), shapes[i]
+
+
+def test_fused_large_batch_of_tiny_matrices():
+    """65 537 matrices of 3 x 5 in one batched call: one workgroup each in one
+    launch, bitwise the tiled kernels."""
+    g = torch.Generator(device="cuda")
+    g.manual_seed(5)
+    X = torch.randn((65537, 3, 5), generator=g, device="cuda").bfloat16()
+    f = X.clone()
+    counts = launches(lambda: tm.orthogonalize(f, 4, None, "aol"))
+    assert only_fused(counts), counts
+    t = X.clone()
+    with tiled_only():
+        tm.orthogonalize(t, 4, None, "aol")
+        torch.cuda.synchronize()
+    assert torch.equal(f.view(torch.int16), t.view(torch.int16))
+    e = relF(from_device(f[65536]), O.orthogonalize(from_device(X[65536]), 4, None, "aol"))
+    assert e <= BF16_TOL
