@@ -321,6 +321,25 @@ def test_grouped_mixed_k_dealt_by_matrix_matches_single_calls():
         assert e <= BF16_TOL
 
 
+@pytest.mark.parametrize("precond", ["schatten4", "aol", "frobenius"])
+def test_small_matrix_alone_and_beside_large_ones_bitwise(precond):
+    """A 100 x 300 matrix alone (fused kernel) and in a group with two 2048 x 8192
+    matrices (tiled kernels on 256 x 256 tiles, its rows padded to 256): the same
+    bits.  The Schatten-4 sums are chunked by the 64-column partials of the k real
+    rows, not of the padded width, so the tile size does not enter them."""
+    log(f"case: 100x300 alone vs beside 2 x 2048x8192, {precond}")
+    small = make_input(100, 300, 0.8, 41, "bf16")
+    big = [make_input(2048, 8192, 0.5, 42 + i, "bf16") for i in range(2)]
+    alone = to_device(small, "bf16")
+    tm.orthogonalize(alone, 4, None, precond)
+    ts = [to_device(small, "bf16")] + [to_device(b, "bf16") for b in big]
+    tm.orthogonalize_grouped(ts, 4, None, precond)
+    torch.cuda.synchronize()
+    assert torch.equal(alone, ts[0])
+    e = relF(from_device(ts[0]), O.orthogonalize(small, 4, None, precond))
+    assert e <= BF16_TOL
+
+
 def test_grouped_resnet_conv_64_matrices():
     log("case: grouped resnet_conv_64 (64 matrices)")
     Xs, Gs = run_workload("resnet_conv_64")
