@@ -132,6 +132,8 @@ def test_larger_call_after_capture_keeps_the_graph_valid():
     del graph
 
 
+# the refused call enqueues nothing, so torch reports the captured graph as empty
+@pytest.mark.filterwarnings("ignore:The CUDA Graph is empty")
 def test_capture_with_too_small_a_workspace_is_refused():
     """Nothing can be allocated during capture: a call whose stream has no workspace
     of that size yet returns TM_ERR_UNSUPPORTED and enqueues nothing."""
