@@ -112,6 +112,24 @@ __device__ inline uint16_t half_of(const uint4& v, int t) {
   return uint16_t(w >> (16 * (t & 1)));
 }
 
+__device__ inline uint32_t word_of(const uint4& v, int d) {
+  return d == 0 ? v.x : (d == 1 ? v.y : (d == 2 ? v.z : v.w));
+}
+
+// 8 x 8 block of 16-bit elements, rows in[r] (element c = half c % 2 of word
+// c / 2): out[c] = column c, its element r from in[r].
+__device__ inline void transpose8(const uint4 (&in)[8], uint4 (&out)[8]) {
+#pragma unroll
+  for (int c = 0; c < 8; ++c) {
+    const uint32_t sel = (c & 1) ? 0x07060302u : 0x05040100u;
+    uint32_t w[4];
+#pragma unroll
+    for (int d = 0; d < 4; ++d)
+      w[d] = __builtin_amdgcn_perm(word_of(in[2 * d + 1], c >> 1), word_of(in[2 * d], c >> 1), sel);
+    out[c] = make_uint4(w[0], w[1], w[2], w[3]);
+  }
+}
+
 // Y = the wide view of X (X itself, or X^T for a tall matrix), zero padded.
 // Each thread issues LB loads before it stores any of them; a load outside
 // the matrix reads X's first element instead and its value is replaced by
@@ -169,6 +187,27 @@ __device__ inline void load_y(const Geo& G, const uint16_t* X, bool tall) {
         }
       }
     }
+  } else if (vec && (G.k % 8) == 0) {
+    // 8 x 8 blocks of the padded Y: 8 rows of X (8 elements each) are loaded,
+    // transposed in registers and written as 8 16-byte row pieces of Y
+    const int nbi = G.kp / 8;
+    const int total = (G.Np / 8) * nbi;
+    const Div dv{uint32_t(nbi)};
+    for (int q = tid; q < total; q += NT) {
+      const int lb = int(dv(uint32_t(q))), i0 = (q - lb * nbi) * 8, l0 = lb * 8;
+      uint4 v[8];
+#pragma unroll
+      for (int r = 0; r < 8; ++r) {
+        const bool ok = l0 + r < G.N && i0 < G.k;
+        const uint4 x = *reinterpret_cast<const uint4*>(X + (ok ? int64_t(l0 + r) * G.k + i0 : 0));
+        const uint32_t m = ok ? ~0u : 0u;
+        v[r] = make_uint4(x.x & m, x.y & m, x.z & m, x.w & m);
+      }
+      uint4 o[8];
+      transpose8(v, o);
+#pragma unroll
+      for (int c = 0; c < 8; ++c) *reinterpret_cast<uint4*>(G.y + (i0 + c) * G.ry + l0 * 2) = o[c];
+    }
   } else {
     const int cpr = G.Np / 8;
     for (int q = tid; q < G.kp * cpr; q += NT) {   // zero fill, then scatter the columns
@@ -179,26 +218,20 @@ __device__ inline void load_y(const Geo& G, const uint16_t* X, bool tall) {
     const int ck = (G.k + 7) / 8;                  // 8-element pieces of an X row
     const int total = G.N * ck;
     const Div dv{uint32_t(ck)};
-    const bool colvec = vec && (G.k % 8) == 0;
     for (int q0 = tid; q0 < total; q0 += LB * NT) {
       uint4 v[LB];
 #pragma unroll
       for (int u = 0; u < LB; ++u) {
         const int q = q0 + u * NT;
         const int l = int(dv(uint32_t(q))), i0 = (q - l * ck) * 8;
-        if (colvec) {
-          const bool ok = q < total;
-          v[u] = *reinterpret_cast<const uint4*>(X + (ok ? int64_t(l) * G.k + i0 : 0));
-        } else {
-          uint32_t h[4];
+        uint32_t h[4];
 #pragma unroll
-          for (int t = 0; t < 8; ++t) {
-            const bool ok = q < total && i0 + t < G.k;
-            const uint32_t x = uint32_t(X[ok ? int64_t(l) * G.k + i0 + t : 0]) << (16 * (t & 1));
-            h[t >> 1] = (t & 1) ? (h[t >> 1] | x) : x;
-          }
-          v[u] = make_uint4(h[0], h[1], h[2], h[3]);
+        for (int t = 0; t < 8; ++t) {
+          const bool ok = q < total && i0 + t < G.k;
+          const uint32_t x = uint32_t(X[ok ? int64_t(l) * G.k + i0 + t : 0]) << (16 * (t & 1));
+          h[t >> 1] = (t & 1) ? (h[t >> 1] | x) : x;
         }
+        v[u] = make_uint4(h[0], h[1], h[2], h[3]);
       }
 #pragma unroll
       for (int u = 0; u < LB; ++u) {
@@ -248,11 +281,27 @@ __device__ inline void store_y(const Geo& G, uint16_t* X, bool tall) {
         }
       }
     }
+  } else if (vec && (G.k % 8) == 0) {
+    // 8 x 8 blocks: 8 16-byte row pieces of Y read, transposed in registers,
+    // stored as 8 rows of X
+    const int nbi = G.k / 8;
+    const int total = ((G.N + 7) / 8) * nbi;
+    const Div dv{uint32_t(nbi)};
+    for (int q = tid; q < total; q += NT) {
+      const int lb = int(dv(uint32_t(q))), i0 = (q - lb * nbi) * 8, l0 = lb * 8;
+      uint4 v[8];
+#pragma unroll
+      for (int c = 0; c < 8; ++c) v[c] = *reinterpret_cast<const uint4*>(G.y + (i0 + c) * G.ry + l0 * 2);
+      uint4 o[8];
+      transpose8(v, o);
+#pragma unroll
+      for (int r = 0; r < 8; ++r)
+        if (l0 + r < G.N) *reinterpret_cast<uint4*>(X + int64_t(l0 + r) * G.k + i0) = o[r];
+    }
   } else {
     const int ck = (G.k + 7) / 8;
     const int total = G.N * ck;
     const Div dv{uint32_t(ck)};
-    const bool colvec = vec && (G.k % 8) == 0;
     for (int q0 = tid; q0 < total; q0 += LB * NT) {
       uint4 e[LB];
 #pragma unroll
@@ -274,13 +323,9 @@ __device__ inline void store_y(const Geo& G, uint16_t* X, bool tall) {
         const int l = int(dv(uint32_t(q))), i0 = (q - l * ck) * 8;
         if (q >= total) continue;
         uint16_t* dst = X + int64_t(l) * G.k + i0;
-        if (colvec) {
-          *reinterpret_cast<uint4*>(dst) = e[u];
-        } else {
 #pragma unroll
-          for (int t = 0; t < 8; ++t)
-            if (i0 + t < G.k) dst[t] = half_of(e[u], t);
-        }
+        for (int t = 0; t < 8; ++t)
+          if (i0 + t < G.k) dst[t] = half_of(e[u], t);
       }
     }
   }
@@ -289,9 +334,10 @@ __device__ inline void store_y(const Geo& G, uint16_t* X, bool tall) {
 // acc = R R^T over K (16-byte rows of R at row stride rb, K a multiple of 32):
 // wave (wm, wn) owns the F x F blocks of 16 x 16 at rows wm 16 F + 16 fm,
 // columns wn 16 F + 16 fn.  Element v of block (fm, fn) is row 4 (L / 16) + v,
-// column L % 16 of the block.  The fragments of the next 32-wide K slice are
-// read while the current one multiplies; the read after the last slice lands
-// in the row padding or the next region of the LDS and is discarded.
+// column L % 16 of the block.  The fragments of the K slice two ahead are
+// read while the current one multiplies (three fragment sets in rotation);
+// the reads past the last slice land in the next row or the next region of
+// the LDS (at most 128 bytes past a row's data) and are discarded.
 template <int F>
 __device__ inline void sym_product(f32x4_t (&acc)[F][F], const char* R, int rb, int K) {
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
@@ -316,16 +362,20 @@ __device__ inline void sym_product(f32x4_t (&acc)[F][F], const char* R, int rb, 
 #pragma unroll
       for (int fn = 0; fn < F; ++fn) acc[fm][fn] = mfma(fa[fm], fb[fn], acc[fm][fn]);
   };
-  uint4 a0[F], b0[F], a1[F], b1[F];
+  uint4 a0[F], b0[F], a1[F], b1[F], a2[F], b2[F];
   fetch(a0, b0, 0);
+  fetch(a1, b1, 32);
   int k0 = 0;
-  for (; k0 + 64 <= K; k0 += 64) {
-    fetch(a1, b1, k0 + 32);
+  for (; k0 + 96 <= K; k0 += 96) {
+    fetch(a2, b2, k0 + 64);
     mult(a0, b0);
-    fetch(a0, b0, k0 + 64);
+    fetch(a0, b0, k0 + 96);
     mult(a1, b1);
+    fetch(a1, b1, k0 + 128);
+    mult(a2, b2);
   }
   if (k0 < K) mult(a0, b0);
+  if (k0 + 32 < K) mult(a1, b1);
 }
 
 template <int F>
