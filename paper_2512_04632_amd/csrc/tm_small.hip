@@ -218,10 +218,11 @@ __device__ inline void load_y(const Geo& G, const uint16_t* X, bool tall) {
     const int ck = (G.k + 7) / 8;                  // 8-element pieces of an X row
     const int total = G.N * ck;
     const Div dv{uint32_t(ck)};
-    for (int q0 = tid; q0 < total; q0 += LB * NT) {
-      uint4 v[LB];
+    constexpr int LE = LB / 2;   // pieces in flight: 8 element loads each
+    for (int q0 = tid; q0 < total; q0 += LE * NT) {
+      uint4 v[LE];
 #pragma unroll
-      for (int u = 0; u < LB; ++u) {
+      for (int u = 0; u < LE; ++u) {
         const int q = q0 + u * NT;
         const int l = int(dv(uint32_t(q))), i0 = (q - l * ck) * 8;
         uint32_t h[4];
@@ -234,7 +235,7 @@ __device__ inline void load_y(const Geo& G, const uint16_t* X, bool tall) {
         v[u] = make_uint4(h[0], h[1], h[2], h[3]);
       }
 #pragma unroll
-      for (int u = 0; u < LB; ++u) {
+      for (int u = 0; u < LE; ++u) {
         const int q = q0 + u * NT;
         const int l = int(dv(uint32_t(q))), i0 = (q - l * ck) * 8;
         if (q < total) {
@@ -334,10 +335,10 @@ __device__ inline void store_y(const Geo& G, uint16_t* X, bool tall) {
 // acc = R R^T over K (16-byte rows of R at row stride rb, K a multiple of 32):
 // wave (wm, wn) owns the F x F blocks of 16 x 16 at rows wm 16 F + 16 fm,
 // columns wn 16 F + 16 fn.  Element v of block (fm, fn) is row 4 (L / 16) + v,
-// column L % 16 of the block.  The fragments of the K slice two ahead are
-// read while the current one multiplies (three fragment sets in rotation);
-// the reads past the last slice land in the next row or the next region of
-// the LDS (at most 128 bytes past a row's data) and are discarded.
+// column L % 16 of the block.  The fragments of the K slice two ahead (one
+// ahead for F = 1) are read while the current one multiplies; the reads past
+// the last slice land in the next row or the next region of the LDS (at most
+// 128 bytes past a row's data) and are discarded.
 template <int F>
 __device__ inline void sym_product(f32x4_t (&acc)[F][F], const char* R, int rb, int K) {
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
@@ -362,20 +363,31 @@ __device__ inline void sym_product(f32x4_t (&acc)[F][F], const char* R, int rb, 
 #pragma unroll
       for (int fn = 0; fn < F; ++fn) acc[fm][fn] = mfma(fa[fm], fb[fn], acc[fm][fn]);
   };
-  uint4 a0[F], b0[F], a1[F], b1[F], a2[F], b2[F];
+  uint4 a0[F], b0[F], a1[F], b1[F];
   fetch(a0, b0, 0);
-  fetch(a1, b1, 32);
   int k0 = 0;
-  for (; k0 + 96 <= K; k0 += 96) {
-    fetch(a2, b2, k0 + 64);
-    mult(a0, b0);
-    fetch(a0, b0, k0 + 96);
-    mult(a1, b1);
-    fetch(a1, b1, k0 + 128);
-    mult(a2, b2);
+  if constexpr (F == 1) {   // one slice ahead: a third set would halve the blocks per compute unit
+    for (; k0 + 64 <= K; k0 += 64) {
+      fetch(a1, b1, k0 + 32);
+      mult(a0, b0);
+      fetch(a0, b0, k0 + 64);
+      mult(a1, b1);
+    }
+    if (k0 < K) mult(a0, b0);
+  } else {
+    uint4 a2[F], b2[F];
+    fetch(a1, b1, 32);
+    for (; k0 + 96 <= K; k0 += 96) {
+      fetch(a2, b2, k0 + 64);
+      mult(a0, b0);
+      fetch(a0, b0, k0 + 96);
+      mult(a1, b1);
+      fetch(a1, b1, k0 + 128);
+      mult(a2, b2);
+    }
+    if (k0 < K) mult(a0, b0);
+    if (k0 + 32 < K) mult(a1, b1);
   }
-  if (k0 < K) mult(a0, b0);
-  if (k0 + 32 < K) mult(a1, b1);
 }
 
 template <int F>
