@@ -659,31 +659,21 @@ __global__ __launch_bounds__(64 * NW) void k_small_ns(const SmallPhase P) {
               *reinterpret_cast<const uint2*>(o);
         }
       };
-      // The fragments of the wave's next block are read while the current
-      // one multiplies; with one wave per SIMD, two blocks (c, c + NW) per
-      // step, the first one's results converted and stored while the second
-      // one's products run.  Reads past the last block land in the row
-      // padding or the next LDS region and are discarded.
+      // Two blocks (c, c + NW) per step: the fragments of the wave's next
+      // block are read while the current one multiplies, and the first
+      // block's results are converted and stored while the second one's
+      // products run.  Reads past the last block land in the row padding or
+      // the next LDS region and are discarded.
       uint4 ya[F], yb[F];
       f32x4_t ua[FR], ub[FR];
       yfrag(ya, w);
-      if constexpr (NW == 8) {
-        for (int c = w; c < nblk; c += NW) {
-          yfrag(yb, c + NW);
-          mult(ua, ya);
-          put(ua, c);
-#pragma unroll
-          for (int s = 0; s < F; ++s) ya[s] = yb[s];
-        }
-      } else {
-        for (int c = w; c < nblk; c += 2 * NW) {
-          yfrag(yb, c + NW);
-          mult(ua, ya);
-          yfrag(ya, c + 2 * NW);
-          mult(ub, yb);
-          put(ua, c);
-          if (c + NW < nblk) put(ub, c + NW);
-        }
+      for (int c = w; c < nblk; c += 2 * NW) {
+        yfrag(yb, c + NW);
+        mult(ua, ya);
+        yfrag(ya, c + 2 * NW);
+        mult(ub, yb);
+        put(ua, c);
+        if (c + NW < nblk) put(ub, c + NW);
       }
     }
     __syncthreads();
