@@ -15,9 +15,12 @@
 //                    iteration 1 the rescaled X1 = diag(s) X0 is folded in
 //   k_apply_scale    iters = 0: X1 = diag(s) X0 in place
 //
+// These are the fp32 path's kernels; a bf16 call runs only the elementwise
+// ones from here (Frobenius partials, AOL vector, iters = 0 rescale) and its
+// matrix-core phases in tm_fast.hip.
+//
 // Matrix-core tiles: 256 threads = 4 wave64s in a 2 x 2 grid; each wave owns
-// (BM/2) x (BN/2) of the output as 32 x 32 MFMA blocks
-// (v_mfma_f32_32x32x16_bf16, or v_mfma_f32_32x32x2_f32 for fp32 storage).
+// (BM/2) x (BN/2) of the output as 32 x 32 MFMA blocks (v_mfma_f32_32x32x2_f32).
 // K advances by 128 bytes per step through double-buffered LDS; global loads
 // of step k+1 are issued before the MFMAs of step k.
 #include <hip/hip_runtime.h>
@@ -29,7 +32,6 @@
 
 namespace tmk {
 
-typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x16_t __attribute__((ext_vector_type(16)));
 
 // ---------------------------------------------------------------- elements
@@ -253,6 +255,7 @@ struct TLoad {
 template <typename T, class C>
 __device__ inline void mma_stage(f32x16_t (&acc)[C::FM][C::FN], const char* ldsA,
                                  const char* ldsB, int wm, int wn) {
+  static_assert(sizeof(T) == 4, "bf16 products run in tm_fast.hip");
   const int lane = threadIdx.x & 63;
   const int lr = lane & 31, lh = lane >> 5;
 #pragma unroll
@@ -270,20 +273,14 @@ __device__ inline void mma_stage(f32x16_t (&acc)[C::FM][C::FN], const char* ldsA
     for (int fm = 0; fm < C::FM; ++fm)
 #pragma unroll
       for (int fn = 0; fn < C::FN; ++fn) {
-        if constexpr (sizeof(T) == 2) {
-          acc[fm][fn] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-              __builtin_bit_cast(bf16x8_t, a[fm]), __builtin_bit_cast(bf16x8_t, b[fn]),
-              acc[fm][fn], 0, 0, 0);
-        } else {
-          // Lanes 0-31 hold k = 0..3 and lanes 32-63 k = 4..7 of the 8-wide K
-          // chunk; both operands share the assignment, so the 4 rank-2 MFMAs
-          // sum the chunk exactly once.
-          const float* af = reinterpret_cast<const float*>(&a[fm]);
-          const float* bf = reinterpret_cast<const float*>(&b[fn]);
+        // Lanes 0-31 hold k = 0..3 and lanes 32-63 k = 4..7 of the 8-wide K
+        // chunk; both operands share the assignment, so the 4 rank-2 MFMAs
+        // sum the chunk exactly once.
+        const float* af = reinterpret_cast<const float*>(&a[fm]);
+        const float* bf = reinterpret_cast<const float*>(&b[fn]);
 #pragma unroll
-          for (int q = 0; q < 4; ++q)
-            acc[fm][fn] = __builtin_amdgcn_mfma_f32_32x32x2f32(af[q], bf[q], acc[fm][fn], 0, 0, 0);
-        }
+        for (int q = 0; q < 4; ++q)
+          acc[fm][fn] = __builtin_amdgcn_mfma_f32_32x32x2f32(af[q], bf[q], acc[fm][fn], 0, 0, 0);
       }
   }
 }
@@ -393,8 +390,7 @@ __device__ inline void store_sym(const f32x16_t (&acc)[C::FM][C::FN], T* __restr
           for (int u = 0; u < 4; ++u) out[u] = Elem<T>::from_f(g(ib + u, j, acc[fm][fn][4 * v4 + u]));
           T* p = D + int64_t(j) * ld + ib;
           if (ib + 3 < k) {
-            if constexpr (sizeof(T) == 2) *reinterpret_cast<uint2*>(p) = *reinterpret_cast<uint2*>(out);
-            else *reinterpret_cast<uint4*>(p) = *reinterpret_cast<uint4*>(out);
+            *reinterpret_cast<uint4*>(p) = *reinterpret_cast<uint4*>(out);
           } else {
             for (int u = 0; u < 4; ++u)
               if (ib + u < k) p[u] = out[u];
