@@ -83,7 +83,10 @@ def test_fused_matches_oracle(m, n, precond, iters):
 
 
 SHAPES = [(1, 1), (3, 5), (5, 3), (17, 33), (33, 17), (31, 32), (32, 31), (64, 576), (576, 64),
-          (65, 129), (129, 65), (127, 200), (128, 320), (8, 1000)]
+          (65, 129), (129, 65), (127, 200), (128, 320), (8, 1000),
+          # tall with k % 8 == 0 (8 x 8 register-transposed loads and stores): a last
+          # block of 8 rows only partly inside the matrix, zero columns past N
+          (333, 40), (99, 8), (200, 96)]
 CASES = [("aol", 4, None), ("aol", 1, None), ("frobenius", 5, None), ("schatten4", 4, None),
          ("none", 3, None), ("aol", 5, SCHEDULE5)]
 
