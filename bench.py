@@ -172,7 +172,7 @@ def main(argv=None) -> int:
     torch.cuda.synchronize()
     tm.timing_enable(False)
     elapsed_ms = start.elapsed_time(stop)
-    phase_names = ("load_in", "frob", "gram", "aol_vector", "scale_a", "poly", "update")
+    phase_names = ("load_in", "frob", "gram", "aol_vector", "scale_a", "poly", "update", "fused")
     phases = {p: tm.timing_read(p) for p in phase_names}
     progress(f"timed {args.steps} steps: {elapsed_ms:.3f} ms")
 
@@ -229,6 +229,18 @@ def main(argv=None) -> int:
                                "k_update_fast launch of the timed steps (library timing hooks); "
                                "achieved = update flops of those launches / their summed time"},
     }
+    fused_ms, fused_n = phases["fused"]
+    if not upd_n and fused_n:
+        # every phase and iteration of a call in one k_small_ns launch per call
+        fl_fused = step_flops * args.steps / (fused_ms * 1e-3) / 1e12
+        result["roofline"] = {
+            "bound": "mfma", "kernel": "k_small_ns", "achieved": round(fl_fused, 2), "peak": peak,
+            "unit": "TFLOP/s", "frac": round(fl_fused / peak, 4), "traffic": None,
+            "launch_avg_ms": round(fused_ms / fused_n, 4), "launches": fused_n,
+            "flops_per_launch": step_flops * args.steps // fused_n,
+            "source": "HIP events recorded on the call's stream around every k_small_ns launch "
+                      "of the timed steps (library timing hooks; one launch runs a whole call); "
+                      "achieved = the calls' algorithmic flops / the launches' summed time"}
 
     if not args.no_cpu_baseline:
         # The cpu_baseline leg: the oracle timed on the host cores; its results
