@@ -302,13 +302,13 @@ def main(argv=None) -> int:
 # sub-records of the default line: (label, workload, iters, precond).  The
 # 4096 x 14336 half of the 8B-class configuration is the line itself.
 CONFIGS = [
-    ("c1", "single_256_f32", 4, "aol"),
-    ("c2", "gpt2_mlp_768x3072", 4, "aol"),
-    ("c2_muon", "gpt2_mlp_768x3072", 5, "frobenius"),
-    ("c3", "gpt2_small_12layer", 4, "aol"),
-    ("c4_4096x4096", "llm8b_4096x4096_b8", 4, "aol"),
-    ("c5", "resnet_conv_64", 4, "aol"),
-    ("c5_64x576", "resnet_conv_64x576_b16", 4, "aol"),
+    ("single_256_f32", "single_256_f32", 4, "aol"),
+    ("gpt2_mlp_768x3072", "gpt2_mlp_768x3072", 4, "aol"),
+    ("gpt2_mlp_768x3072_muon", "gpt2_mlp_768x3072", 5, "frobenius"),
+    ("gpt2_small_12layer", "gpt2_small_12layer", 4, "aol"),
+    ("llm8b_4096x4096_b8", "llm8b_4096x4096_b8", 4, "aol"),
+    ("resnet_conv_64", "resnet_conv_64", 4, "aol"),
+    ("resnet_conv_64x576_b16", "resnet_conv_64x576_b16", 4, "aol"),
 ]
 
 
@@ -409,7 +409,7 @@ def _config_records(args, dev, progress):
                         "rel_frobenius_vs_oracle": float(O.rel_frobenius(G, R)),
                         "eps_ortho_gpu": float(O.eps_ortho(G)),
                         "eps_ortho_oracle": float(O.eps_ortho(R))}
-                if label == "c1":   # the accuracy configuration: distance to the SVD polar factor
+                if label == "single_256_f32":   # the accuracy configuration: distance to the SVD polar factor
                     Q = O.polar_factor(Xh)
                     item["eps_polar_gpu"] = float(O.eps_polar(G, Xh, Q))
                     item["eps_polar_oracle"] = float(O.eps_polar(R, Xh, Q))
